@@ -1,0 +1,227 @@
+/*
+ * oracle_attn.c -- CPU oracle for decode-step grouped-query attention over
+ * ragged per-sequence KV caches.
+ *
+ * TEST INFRASTRUCTURE ONLY.  Nothing in the product library links, loads or
+ * calls this file; only the tests, the smoke check and the benchmark's CPU
+ * baseline do.  It shares no code, header or constant with the HIP path.
+ *
+ * What it computes (one decode step of the student's rollout):
+ *   each in-flight request b decodes one new token whose query heads attend
+ *   over that request's token context c_{t,j} = c_t + x_{t,<j}
+ *   (Sec. 3, eq:token-context), i.e. the request's cached K/V rows.  For the
+ *   reference-conditioned fast action the context is c_t + o^ref_{t+1}
+ *   (Sec. 4.1, eq:reference-conditioned-action); for NAP and full responses
+ *   it is c_t (eq:autonomous-action, eq:agent-response).  Inputs are bf16,
+ *   the paper's rollout precision (tab:training-hyperparameters).
+ *
+ * The paper does not write out the attention formula; this file follows the
+ * standard softmax attention definition, for every b < B and h < Hq:
+ *   kv   = floor(h / g),  g = Hq / Hkv      (consecutive query heads share a KV head)
+ *   r_t  = seq_offsets[b] + t,  t < L_b = seq_lens[b]
+ *   s_t  = scale * sum_d q[b,h,d] * K[r_t,kv,d]
+ *   w_t  = exp(s_t) / sum_u exp(s_u)
+ *   out[b,h,d] = sum_t w_t * V[r_t,kv,d]          (L_b = 0 gives zeros)
+ * computed in two plain passes in double precision.  Subtracting max_t s_t
+ * before exp leaves every w_t unchanged (it cancels between numerator and
+ * denominator) and only keeps exp in range.  No blocking, splitting or
+ * online rescaling is done here.
+ *
+ * Memory layout (all arrays on the host, row-major):
+ *   q    uint16 bf16 bits [B, Hq, D]
+ *   K, V uint16 bf16 bits [num_rows, Hkv, D]
+ *   out  double [B, Hq, D]
+ * Parity: pinned (closed forms, brute force, invariants; see the tests).
+ */
+#include <math.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+
+#ifdef _OPENMP
+#include <omp.h>
+#endif
+
+#define ORACLE_OK 0
+#define ORACLE_ERR_ARG -1
+#define ORACLE_ERR_RANGE -2
+#define ORACLE_ERR_NOMEM -3
+
+/* bfloat16 bits -> value: the bf16 pattern is the upper half of a float32. */
+static double bf16_value(uint16_t bits)
+{
+    uint32_t u = (uint32_t)bits << 16;
+    float f;
+    memcpy(&f, &u, sizeof f);
+    return (double)f;
+}
+
+static int check_shape(int32_t num_seqs, int32_t hq, int32_t hkv, int32_t d)
+{
+    if (num_seqs < 0 || hq <= 0 || hkv <= 0 || d <= 0)
+        return ORACLE_ERR_ARG;
+    if (hq % hkv != 0)
+        return ORACLE_ERR_ARG;
+    return ORACLE_OK;
+}
+
+/*
+ * Attention weights w_t of one (sequence, query head): the softmax of the
+ * scaled logits over the sequence's rows.  Writes L_b doubles to w.
+ */
+static int weights_one(const uint16_t *q, const uint16_t *k,
+                       const int32_t *seq_offsets, const int32_t *seq_lens,
+                       int32_t b, int32_t h, int32_t hq, int32_t hkv, int32_t d,
+                       int64_t num_rows, double scale, double *w)
+{
+    const int32_t g = hq / hkv;
+    const int32_t kv = h / g;
+    const int64_t off = seq_offsets[b];
+    const int64_t len = seq_lens[b];
+    if (len < 0 || off < 0 || off + len > num_rows)
+        return ORACLE_ERR_RANGE;
+    if (len == 0)
+        return ORACLE_OK;
+
+    const uint16_t *qrow = q + ((int64_t)b * hq + h) * d;
+    double smax = -INFINITY;
+    for (int64_t t = 0; t < len; ++t) {
+        const uint16_t *krow = k + ((off + t) * hkv + kv) * d;
+        double dot = 0.0;
+        for (int32_t i = 0; i < d; ++i)
+            dot += bf16_value(qrow[i]) * bf16_value(krow[i]);
+        w[t] = scale * dot;
+        if (w[t] > smax)
+            smax = w[t];
+    }
+    double z = 0.0;
+    for (int64_t t = 0; t < len; ++t) {
+        w[t] = exp(w[t] - smax);
+        z += w[t];
+    }
+    for (int64_t t = 0; t < len; ++t)
+        w[t] /= z;
+    return ORACLE_OK;
+}
+
+/* out[d] = sum_t w_t V[r_t, kv, :] for one (sequence, query head). */
+static int attend_one(const uint16_t *q, const uint16_t *k, const uint16_t *v,
+                      const int32_t *seq_offsets, const int32_t *seq_lens,
+                      int32_t b, int32_t h, int32_t hq, int32_t hkv, int32_t d,
+                      int64_t num_rows, double scale, double *w, double *out)
+{
+    const int32_t kv = h / (hq / hkv);
+    for (int32_t i = 0; i < d; ++i)
+        out[i] = 0.0;
+    int rc = weights_one(q, k, seq_offsets, seq_lens, b, h, hq, hkv, d, num_rows, scale, w);
+    if (rc != ORACLE_OK)
+        return rc;
+    const int64_t off = seq_offsets[b];
+    const int64_t len = seq_lens[b];
+    for (int64_t t = 0; t < len; ++t) {
+        const uint16_t *vrow = v + ((off + t) * hkv + kv) * d;
+        for (int32_t i = 0; i < d; ++i)
+            out[i] += w[t] * bf16_value(vrow[i]);
+    }
+    return ORACLE_OK;
+}
+
+static int64_t max_len(const int32_t *seq_lens, int32_t n)
+{
+    int64_t m = 0;
+    for (int32_t i = 0; i < n; ++i)
+        if (seq_lens[i] > m)
+            m = seq_lens[i];
+    return m;
+}
+
+/*
+ * Selected (sequence, query head) pairs: pairs[2*i] = b, pairs[2*i+1] = h,
+ * out[i*D .. i*D+D) receives that head's output.  Runs the pairs in parallel
+ * over num_threads OpenMP threads (<= 0: the OpenMP default).
+ */
+int oracle_decode_attn_pairs(const uint16_t *q, const uint16_t *k, const uint16_t *v,
+                             const int32_t *seq_offsets, const int32_t *seq_lens,
+                             int32_t num_seqs, int32_t hq, int32_t hkv, int32_t d,
+                             int64_t num_rows, double scale,
+                             const int32_t *pairs, int64_t num_pairs,
+                             double *out, int32_t num_threads)
+{
+    int rc = check_shape(num_seqs, hq, hkv, d);
+    if (rc != ORACLE_OK)
+        return rc;
+    for (int64_t i = 0; i < num_pairs; ++i)
+        if (pairs[2 * i] < 0 || pairs[2 * i] >= num_seqs || pairs[2 * i + 1] < 0 ||
+            pairs[2 * i + 1] >= hq)
+            return ORACLE_ERR_ARG;
+    const int64_t lmax = max_len(seq_lens, num_seqs);
+    int status = ORACLE_OK;
+#ifdef _OPENMP
+    if (num_threads <= 0)
+        num_threads = omp_get_max_threads();
+#pragma omp parallel num_threads(num_threads)
+#endif
+    {
+        double *w = (double *)malloc((size_t)(lmax > 0 ? lmax : 1) * sizeof(double));
+        if (w == NULL) {
+#ifdef _OPENMP
+#pragma omp atomic write
+#endif
+            status = ORACLE_ERR_NOMEM;
+        }
+#ifdef _OPENMP
+#pragma omp for schedule(dynamic, 1)
+#endif
+        for (int64_t i = 0; i < num_pairs; ++i) {
+            if (w == NULL)
+                continue;
+            int r = attend_one(q, k, v, seq_offsets, seq_lens, pairs[2 * i], pairs[2 * i + 1],
+                               hq, hkv, d, num_rows, scale, w, out + i * d);
+            if (r != ORACLE_OK) {
+#ifdef _OPENMP
+#pragma omp atomic write
+#endif
+                status = r;
+            }
+        }
+        free(w);
+    }
+    return status;
+}
+
+/* Every (sequence, query head): out is [num_seqs, Hq, D]. */
+int oracle_decode_attn(const uint16_t *q, const uint16_t *k, const uint16_t *v,
+                       const int32_t *seq_offsets, const int32_t *seq_lens,
+                       int32_t num_seqs, int32_t hq, int32_t hkv, int32_t d,
+                       int64_t num_rows, double scale, double *out, int32_t num_threads)
+{
+    int rc = check_shape(num_seqs, hq, hkv, d);
+    if (rc != ORACLE_OK)
+        return rc;
+    const int64_t n = (int64_t)num_seqs * hq;
+    int32_t *pairs = (int32_t *)malloc((size_t)(n > 0 ? n : 1) * 2 * sizeof(int32_t));
+    if (pairs == NULL)
+        return ORACLE_ERR_NOMEM;
+    for (int64_t i = 0; i < n; ++i) {
+        pairs[2 * i] = (int32_t)(i / hq);
+        pairs[2 * i + 1] = (int32_t)(i % hq);
+    }
+    rc = oracle_decode_attn_pairs(q, k, v, seq_offsets, seq_lens, num_seqs, hq, hkv, d,
+                                  num_rows, scale, pairs, n, out, num_threads);
+    free(pairs);
+    return rc;
+}
+
+/* The softmax weights w_t (L_b of them) of one (sequence, query head). */
+int oracle_attn_weights(const uint16_t *q, const uint16_t *k,
+                        const int32_t *seq_offsets, const int32_t *seq_lens,
+                        int32_t num_seqs, int32_t hq, int32_t hkv, int32_t d,
+                        int64_t num_rows, double scale, int32_t b, int32_t h, double *w)
+{
+    int rc = check_shape(num_seqs, hq, hkv, d);
+    if (rc != ORACLE_OK)
+        return rc;
+    if (b < 0 || b >= num_seqs || h < 0 || h >= hq)
+        return ORACLE_ERR_ARG;
+    return weights_one(q, k, seq_offsets, seq_lens, b, h, hq, hkv, d, num_rows, scale, w);
+}

@@ -1,0 +1,332 @@
+"""Pins of the CPU oracle against facts fixed by mathematics, not by the oracle.
+
+Each test names the mistake it is there to catch.  The oracle computes one
+decode step of softmax attention of each request's new token over its token
+context (Sec. 3, eq:token-context), with grouped KV heads.
+"""
+import json
+import math
+import os
+
+import numpy as np
+import pytest
+
+import oracle
+from paper_2609_36608_amd import workloads as wl
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+bf = wl.f32_to_bf16_bits
+unbf = wl.bf16_bits_to_f32
+
+
+def rand_bits(rng, shape, scale=1.0):
+    return bf(rng.standard_normal(shape).astype(np.float32) * np.float32(scale))
+
+
+def single(q, k, v, scale):
+    """One sequence at offset 0 using all rows."""
+    n = k.shape[0]
+    return oracle.decode_attn(q, k, v, np.array([0]), np.array([n]), scale)
+
+
+# ------------------------------------------------------------- closed forms
+
+def test_golden_three_keys():
+    """Hand-derived closed form (weights 1/7, 2/7, 4/7). Catches a sign flip in
+    the softmax, a missing normalisation and wrong q/K pairing."""
+    g = json.load(open(os.path.join(GOLDEN, "three_keys.json")))
+    q = bf(np.array(g["q"], np.float32)).reshape(1, 1, -1)
+    k = bf(np.array(g["k"], np.float32)).reshape(3, 1, -1)
+    v = bf(np.array(g["v"], np.float32)).reshape(3, 1, -1)
+    out = single(q, k, v, g["scale"])[0, 0]
+    np.testing.assert_allclose(out, g["out"], rtol=0, atol=1e-13)
+    w = oracle.attn_weights(q, k, [0], [3], g["scale"], 0, 0)
+    np.testing.assert_allclose(w, g["weights"], rtol=1e-14, atol=0)
+
+
+def test_single_key_returns_its_value_row_exactly():
+    """P1: L = 1 -> weight exp(0)/exp(0) = 1, output is the V row bit for bit.
+    Catches off-by-one lengths (0 rows read) and row/head indexing slips."""
+    rng = np.random.default_rng(1)
+    hq, hkv, d = 8, 2, 128
+    k = rand_bits(rng, (5, hkv, d))
+    v = rand_bits(rng, (5, hkv, d))
+    q = rand_bits(rng, (3, hq, d))
+    offs, lens = np.array([4, 0, 2]), np.array([1, 1, 1])
+    out = oracle.decode_attn(q, k, v, offs, lens, 0.0884)
+    for b in range(3):
+        for h in range(hq):
+            assert np.array_equal(out[b, h], unbf(v[offs[b], h // (hq // hkv)]).astype(np.float64))
+
+
+def test_identical_keys_give_mean_of_values():
+    """P2: equal logits -> uniform weights -> mean of the sequence's V rows."""
+    rng = np.random.default_rng(2)
+    L, d = 37, 128
+    krow = rand_bits(rng, (1, 1, d))
+    k = np.repeat(krow, L, axis=0)
+    v = rand_bits(rng, (L, 1, d))
+    q = rand_bits(rng, (1, 1, d))
+    out = single(q, k, v, 0.3)[0, 0]
+    np.testing.assert_allclose(out, unbf(v[:, 0]).astype(np.float64).mean(axis=0), rtol=0, atol=1e-14)
+
+
+def test_constant_values_are_returned():
+    """P3: V = c everywhere -> out = c, whatever the keys.  Catches weights not
+    summing to one (a dropped or doubled normaliser)."""
+    rng = np.random.default_rng(3)
+    L, d = 300, 128
+    k = rand_bits(rng, (L, 2, d), scale=3.0)
+    v = np.full((L, 2, d), bf(np.array([-1.375], np.float32))[0], dtype=np.uint16)
+    q = rand_bits(rng, (1, 4, d))
+    out = single(q, k, v, 1 / math.sqrt(d))
+    np.testing.assert_allclose(out, -1.375, rtol=1e-14, atol=0)
+
+
+def test_zero_query_averages_exactly_the_sequence_rows():
+    """P4: q = 0 -> uniform weights over rows [off, off + L).  The cache holds
+    other sequences and NaN gaps around it, so reading one row too many, too
+    few or from the wrong offset shows up."""
+    rng = np.random.default_rng(4)
+    d, hkv, hq = 128, 2, 4
+    rows = 64
+    k = rand_bits(rng, (rows, hkv, d))
+    v = rand_bits(rng, (rows, hkv, d))
+    k[:10] = wl.BF16_NAN
+    v[:10] = wl.BF16_NAN
+    k[30:] = wl.BF16_NAN
+    v[30:] = wl.BF16_NAN
+    q = np.zeros((1, hq, d), np.uint16)
+    out = oracle.decode_attn(q, k, v, [10], [20], 0.5)
+    for h in range(hq):
+        expect = unbf(v[10:30, h // 2]).astype(np.float64).mean(axis=0)
+        np.testing.assert_allclose(out[0, h], expect, rtol=0, atol=1e-14)
+
+
+def test_scale_zero_is_uniform_average():
+    """scale = 0 -> all logits 0 -> mean over the rows, whatever q and K."""
+    rng = np.random.default_rng(14)
+    L, d = 50, 128
+    k = rand_bits(rng, (L, 1, d), 4.0)
+    v = rand_bits(rng, (L, 1, d))
+    q = rand_bits(rng, (1, 1, d), 4.0)
+    out = single(q, k, v, 0.0)[0, 0]
+    np.testing.assert_allclose(out, unbf(v[:, 0]).astype(np.float64).mean(axis=0), rtol=0, atol=1e-14)
+
+
+def test_two_keys_designed_logits():
+    """P8: q = 1 in every dim, K row t = x_t in every dim, so
+    s_t = scale * D * x_t without evaluating a dot product here, and
+    out = sigmoid(s0 - s1) v0 + sigmoid(s1 - s0) v1.
+    Catches a dropped dimension (D-1 terms), a missing or squared scale and a
+    sign error in the softmax."""
+    d = 128
+    scale = 1 / math.sqrt(d)
+    rng = np.random.default_rng(8)
+    for x0, x1 in [(0.25, -0.5), (0.0, 0.015625), (-0.75, -0.75), (0.5, 0.125)]:
+        q = np.full((1, 1, d), bf(np.array([1.0], np.float32))[0], np.uint16)
+        k = np.stack([np.full((1, d), bf(np.array([x0], np.float32))[0]),
+                      np.full((1, d), bf(np.array([x1], np.float32))[0])]).astype(np.uint16)
+        v = rand_bits(rng, (2, 1, d))
+        s0, s1 = scale * d * x0, scale * d * x1
+        w0 = 1.0 / (1.0 + math.exp(s1 - s0))
+        w1 = 1.0 / (1.0 + math.exp(s0 - s1))
+        expect = w0 * unbf(v[0, 0]).astype(np.float64) + w1 * unbf(v[1, 0]).astype(np.float64)
+        np.testing.assert_allclose(single(q, k, v, scale)[0, 0], expect, rtol=1e-13, atol=1e-14)
+
+
+def test_query_dim_pairs_with_key_dim():
+    """q = e_j (one-hot), so s_t = scale * K[t, kv, j].  With two keys the
+    output is a sigmoid of K[0,kv,j] - K[1,kv,j]; pairing q's dim j with any
+    other key dim, or reading another KV head's key, changes it."""
+    d, hkv, hq = 128, 2, 4
+    rng = np.random.default_rng(9)
+    k = rand_bits(rng, (2, hkv, d))
+    v = rand_bits(rng, (2, hkv, d))
+    kf = unbf(k).astype(np.float64)
+    vf = unbf(v).astype(np.float64)
+    for j in [0, 1, 63, 64, 127]:
+        q = np.zeros((1, hq, d), np.uint16)
+        q[0, :, j] = bf(np.array([1.0], np.float32))[0]
+        out = oracle.decode_attn(q, k, v, [0], [2], 2.0)
+        for h in range(hq):
+            kv = h // (hq // hkv)
+            s0, s1 = 2.0 * kf[0, kv, j], 2.0 * kf[1, kv, j]
+            w0 = 1.0 / (1.0 + math.exp(s1 - s0))
+            expect = w0 * vf[0, kv] + (1 - w0) * vf[1, kv]
+            np.testing.assert_allclose(out[0, h], expect, rtol=1e-13, atol=1e-14)
+
+
+# ------------------------------------------------------------- invariants
+
+def test_key_value_permutation_invariance():
+    """P5: attention is a set function of the (K, V) rows of a sequence."""
+    rng = np.random.default_rng(5)
+    L, d = 129, 128
+    k = rand_bits(rng, (L, 2, d))
+    v = rand_bits(rng, (L, 2, d))
+    q = rand_bits(rng, (1, 8, d))
+    perm = rng.permutation(L)
+    a = single(q, k, v, 0.1)
+    b = single(q, k[perm], v[perm], 0.1)
+    np.testing.assert_allclose(a, b, rtol=0, atol=1e-14)
+
+
+def test_weights_are_a_distribution():
+    """P6: weights are non-negative and sum to one."""
+    rng = np.random.default_rng(6)
+    L, d = 1000, 128
+    k = rand_bits(rng, (L, 1, d), 2.0)
+    q = rand_bits(rng, (1, 2, d), 2.0)
+    for h in range(2):
+        w = oracle.attn_weights(q, k, [0], [L], 1 / math.sqrt(d), 0, h)
+        assert w.shape == (L,)
+        assert (w >= 0).all()
+        assert abs(w.sum() - 1.0) <= 1e-12
+
+
+def test_values_enter_linearly():
+    """out(2 V) = 2 out(V) exactly (doubling a bf16 is exact)."""
+    rng = np.random.default_rng(15)
+    L, d = 77, 128
+    k = rand_bits(rng, (L, 1, d))
+    v = rand_bits(rng, (L, 1, d))
+    v2 = bf(unbf(v) * np.float32(2.0))
+    q = rand_bits(rng, (1, 2, d))
+    np.testing.assert_array_equal(single(q, k, v2, 0.2), 2.0 * single(q, k, v, 0.2))
+
+
+def test_spike_retrieval_with_huge_logits():
+    """P9: one key per (sequence, KV head) gets a logit about 1000 above the rest,
+    so its V row is returned.  Logits this large also overflow exp() unless the
+    maximum is subtracted first (a missing stabilisation gives NaN)."""
+    rng = np.random.default_rng(10)
+    d, hkv, hq, nseq = 128, 2, 4, 3
+    lens = np.array([40, 17, 64])
+    offs = np.array([100, 0, 20])
+    rows = 140
+    k = rand_bits(rng, (rows, hkv, d), 0.01)
+    # V rows hold codes of (row, kv, dim), exact in bf16
+    code = (np.arange(rows)[:, None, None] * 4 + np.arange(hkv)[None, :, None]) % 251
+    v = bf((code + np.arange(d)[None, None, :] % 3).astype(np.float32))
+    q = np.full((nseq, hq, d), bf(np.array([1.0], np.float32))[0], np.uint16)
+    star = {}
+    for b in range(nseq):
+        for kv in range(hkv):
+            t = int(rng.integers(0, lens[b]))
+            star[(b, kv)] = offs[b] + t
+            k[offs[b] + t, kv] = bf(np.array([96.0], np.float32))[0]
+    out = oracle.decode_attn(q, k, v, offs, lens, 0.0884)
+    assert np.isfinite(out).all()
+    for b in range(nseq):
+        for h in range(hq):
+            kv = h // 2
+            np.testing.assert_allclose(out[b, h], unbf(v[star[(b, kv)], kv]), rtol=0, atol=1e-9)
+
+
+def test_gqa_head_mapping():
+    """P12: V = kv index on each KV head -> out[b, h, :] = floor(h / g).
+    Catches h % Hkv (interleaved) instead of h // g (consecutive) sharing."""
+    rng = np.random.default_rng(12)
+    d, hkv, hq = 128, 4, 16
+    L = 33
+    k = rand_bits(rng, (L, hkv, d))
+    v = np.zeros((L, hkv, d), np.uint16)
+    for kv in range(hkv):
+        v[:, kv] = bf(np.array([float(kv)], np.float32))[0]
+    q = rand_bits(rng, (2, hq, d))
+    out = oracle.decode_attn(q, k, v, [0, 5], [L, L - 5], 0.09)
+    for h in range(hq):
+        np.testing.assert_allclose(out[:, h], float(h // (hq // hkv)), rtol=1e-14, atol=1e-14)
+
+
+def test_placement_independence_and_poison():
+    """P10/P11: a sequence's output depends only on its own rows: shuffled
+    regions with NaN-filled gaps and NaN rows past each length give the same
+    result as each sequence alone at offset 0."""
+    rng = np.random.default_rng(11)
+    w = wl.Workload("t", 90, 1, 5, 8, 2, 3, "uniform", 1, 50)
+    lens = np.array([1, 15, 16, 17, 49], np.int32)
+    lay = wl.make_layout(lens, steps=3, gap_max=7, shuffle=True, rng=rng)
+    k, v = wl.layer_kv_bits(w, lay, 0, fill=wl.BF16_NAN)
+    for b in range(5):  # rows past L_b inside the capacity: poison too
+        k[lay.offsets[b] + lens[b]: lay.offsets[b] + lay.capacity[b]] = wl.BF16_NAN
+        v[lay.offsets[b] + lens[b]: lay.offsets[b] + lay.capacity[b]] = wl.BF16_NAN
+    q = wl.query_bits(w, 0)
+    out = oracle.decode_attn(q, k, v, lay.offsets, lens, w.scale)
+    assert np.isfinite(out).all()
+    for b in range(5):
+        o, L = lay.offsets[b], lens[b]
+        alone = oracle.decode_attn(q[b:b + 1], k[o:o + L], v[o:o + L], [0], [L], w.scale)
+        np.testing.assert_array_equal(out[b], alone[0])
+
+
+def test_empty_sequence_gives_zeros():
+    rng = np.random.default_rng(13)
+    k = rand_bits(rng, (4, 1, 128))
+    v = rand_bits(rng, (4, 1, 128))
+    q = rand_bits(rng, (2, 2, 128))
+    out = oracle.decode_attn(q, k, v, [0, 3], [0, 1], 0.1)
+    assert (out[0] == 0).all()
+    np.testing.assert_array_equal(out[1, 0], unbf(v[3, 0]))
+
+
+def test_rejects_out_of_range_rows():
+    rng = np.random.default_rng(16)
+    k = rand_bits(rng, (4, 1, 128))
+    q = rand_bits(rng, (1, 1, 128))
+    with pytest.raises(ValueError):
+        oracle.decode_attn(q, k, k, [2], [3], 0.1)
+
+
+# ------------------------------------------------------------- brute force
+
+def brute_force(q, k, v, offs, lens, scale):
+    """Pure-Python float64: weights exp(s_t) / sum_u exp(s_u) without the max
+    shift, sums with math.fsum (exactly rounded).  Logits are kept small so
+    the unshifted form cannot overflow."""
+    qf, kf, vf = (unbf(x).astype(np.float64).tolist() for x in (q, k, v))
+    B, hq, d = q.shape
+    hkv = k.shape[1]
+    g = hq // hkv
+    out = np.zeros((B, hq, d))
+    for b in range(B):
+        for h in range(hq):
+            kv = h // g
+            rows = range(offs[b], offs[b] + lens[b])
+            e = [math.exp(scale * math.fsum(qf[b][h][i] * kf[r][kv][i] for i in range(d))) for r in rows]
+            z = math.fsum(e)
+            for i in range(d):
+                out[b, h, i] = math.fsum(e[j] * vf[r][kv][i] for j, r in enumerate(rows)) / z if e else 0.0
+    return out
+
+
+@pytest.mark.parametrize("B,hq,hkv,d", [(1, 2, 1, 4), (3, 4, 2, 4), (2, 4, 1, 128), (3, 2, 2, 128)])
+def test_brute_force_tiny(B, hq, hkv, d):
+    """P7: at tiny sizes the oracle agrees with an independent pure-Python
+    evaluation to 1e-12."""
+    rng = np.random.default_rng(B * 100 + hq * 10 + d)
+    lens = rng.integers(1, 18, size=B)
+    offs = np.concatenate([[0], np.cumsum(lens)[:-1]]) + np.arange(B)
+    rows = int(offs[-1] + lens[-1] + 1)
+    k = rand_bits(rng, (rows, hkv, d))
+    v = rand_bits(rng, (rows, hkv, d))
+    q = rand_bits(rng, (B, hq, d))
+    scale = 1 / math.sqrt(d)
+    np.testing.assert_allclose(oracle.decode_attn(q, k, v, offs, lens, scale),
+                               brute_force(q, k, v, offs, lens, scale), rtol=0, atol=1e-12)
+
+
+def test_threads_do_not_change_results():
+    rng = np.random.default_rng(17)
+    w = wl.WORKLOADS["tiny"]
+    lay = wl.make_layout(wl.draw_lengths(w) // 8, 1)
+    k = rand_bits(rng, (lay.num_rows, w.num_kv_heads, 128))
+    v = rand_bits(rng, (lay.num_rows, w.num_kv_heads, 128))
+    q = wl.query_bits(w, 0)
+    a = oracle.decode_attn(q, k, v, lay.offsets, lay.lens, w.scale, threads=1)
+    b = oracle.decode_attn(q, k, v, lay.offsets, lay.lens, w.scale, threads=4)
+    np.testing.assert_array_equal(a, b)
+    pairs = np.array([[3, 15], [0, 0], [2, 7]])
+    np.testing.assert_array_equal(oracle.decode_attn_pairs(q, k, v, lay.offsets, lay.lens, w.scale, pairs),
+                                  a[pairs[:, 0], pairs[:, 1]])
