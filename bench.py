@@ -1,0 +1,253 @@
+#!/usr/bin/env python3
+"""Benchmark of decode-step GQA attention over ragged multi-turn KV caches on one MI355X.
+
+A step is one decode step of the student's rollout across all layers: for every
+layer, one ctx_decode_attn_run call over the whole batch (every sequence's new
+token attends over its cached context).  Inputs are synthetic, seeded, and
+resident in HBM before the timed region starts.  Prints one JSON line:
+value = algorithmic HBM GB/s of the whole timed region (K and V read once,
+q read, fp32 out written, offsets and lengths), plus decode-steps/s, the
+fraction of the 8 TB/s HBM peak, the roofline of the attention kernel and the
+CPU oracle's rate on a bounded sample of the same workload.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+from paper_2609_36608_amd import workloads as wl  # noqa: E402
+
+METRIC = "decode-attention HBM GB/s (fraction of 8 TB/s peak) + decode-steps/sec, 1 MI355X"
+HBM_PEAK_GBS = 8000.0
+HBM_BUDGET_BYTES = 240 * 2**30  # leave headroom below 288 GB for the rest of the process
+
+
+def algorithmic_bytes(lens: np.ndarray, w: wl.Workload, out_bytes: int = 4) -> int:
+    """K and V rows read once (bf16), q read (bf16), out written, offsets + lengths."""
+    kv = int(lens.astype(np.int64).sum()) * w.num_kv_heads * w.head_dim * 2 * 2
+    b = len(lens)
+    return kv + b * w.num_q_heads * w.head_dim * (2 + out_bytes) + 8 * b
+
+
+def cpu_baseline(w: wl.Workload, layout: wl.Layout, target_s: float, threads: int) -> dict:
+    """Time the CPU oracle on layer 0 / step 0 for a fixed sample of sequences,
+    repeated until about target_s seconds of CPU work have run."""
+    import oracle
+
+    rng = np.random.default_rng(7)
+    lens = layout.lens
+    order = np.argsort(lens)
+    n = min(len(lens), 8)
+    sample = sorted(set([int(order[-1]), int(order[0])] + [int(x) for x in rng.choice(len(lens), n, replace=False)]))[:n]
+    caps = [int(lens[b]) for b in sample]
+    offs = np.concatenate([[0], np.cumsum(caps)[:-1]]).astype(np.int32)
+    k = np.empty((sum(caps), w.num_kv_heads, w.head_dim), np.uint16)
+    v = np.empty_like(k)
+    for i, b in enumerate(sample):
+        kb, vb = wl.sequence_kv_bits(w, 0, b, caps[i])
+        k[offs[i]:offs[i] + caps[i]] = kb
+        v[offs[i]:offs[i] + caps[i]] = vb
+    q = wl.query_bits(w, 0)[sample]
+    sl = np.array(caps, np.int32)
+    nbytes = algorithmic_bytes(sl, w)
+    reps, t0 = 0, time.perf_counter()
+    while True:
+        oracle.decode_attn(q, k, v, offs, sl, w.scale, threads=threads)
+        reps += 1
+        el = time.perf_counter() - t0
+        if el >= target_s or el / reps * (reps + 1) > 3 * target_s:
+            break
+    gbs = nbytes * reps / el / 1e9
+    full_step_bytes = algorithmic_bytes(lens, w) * w.layers
+    return {
+        "value": round(gbs, 4),
+        "unit": "GB/s",
+        "cores": threads,
+        "kind": "oracle",
+        "sample": (f"layer 0, decode step 0, {len(sample)} of {w.batch} sequences "
+                   f"({int(sl.sum())} tokens), all {w.num_q_heads} heads, run {reps}x in {el:.1f} s; "
+                   f"float64 C oracle, OpenMP over (sequence, head)"),
+        "decode_steps_per_s": round(gbs * 1e9 / full_step_bytes, 6),
+    }
+
+
+def main() -> int:
+    ap = argparse.ArgumentParser(description=__doc__)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=64, help="decode steps timed (each = all layers)")
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="long_ragged", choices=sorted(wl.WORKLOADS))
+    ap.add_argument("--graph", action="store_true", help="replay the timed steps from one HIP graph")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    ap.add_argument("--calibrate-copy-gib", type=float, default=0.0,
+                    help="also run one device copy of this many GiB (HBM counter calibration)")
+    args = ap.parse_args()
+
+    if args.gpus != 1:
+        print(f"bench.py: this build measures one GPU only (got --gpus {args.gpus}); the decode "
+              f"attention shards by sequence with no exchange, so run one process per GPU.",
+              file=sys.stderr)
+        return 2
+    if args.steps < 1 or args.warmup < 0:
+        print("bench.py: --steps must be >= 1 and --warmup >= 0", file=sys.stderr)
+        return 2
+
+    import torch
+
+    from paper_2609_36608_amd.binding import DecodeAttention
+
+    if not torch.cuda.is_available():
+        print("bench.py: no GPU visible", file=sys.stderr)
+        return 1
+    dev = torch.device("cuda", 0)
+    torch.cuda.set_device(dev)
+    w = wl.WORKLOADS[args.workload]
+    layout = wl.workload_layout(w)
+    B = w.batch
+
+    # distinct per-layer caches; cycle fewer buffers if all layers exceed HBM
+    layer_bytes = layout.num_rows * w.num_kv_heads * w.head_dim * 2 * 2
+    n_buf = max(1, min(w.layers, HBM_BUDGET_BYTES // layer_bytes))
+    t_setup = time.perf_counter()
+    ks, vs = [], []
+    for i in range(n_buf):
+        k = torch.empty((layout.num_rows, w.num_kv_heads, w.head_dim), dtype=torch.bfloat16, device=dev)
+        v = torch.empty_like(k)
+        wl.fill_normal_bf16_device(k, wl.DEFAULT_SEED, w.index, i, 1)
+        wl.fill_normal_bf16_device(v, wl.DEFAULT_SEED, w.index, i, 2)
+        ks.append(k)
+        vs.append(v)
+    qs = []
+    for layer in range(w.layers):
+        q = torch.empty((B, w.num_q_heads, w.head_dim), dtype=torch.bfloat16, device=dev)
+        wl.fill_normal_bf16_device(q, wl.DEFAULT_SEED, w.index, layer, 0)
+        qs.append(q)
+    outs = [torch.empty((B, w.num_q_heads, w.head_dim), dtype=torch.float32, device=dev) for _ in range(w.layers)]
+    offsets = torch.from_numpy(layout.offsets).to(dev)
+    lens_steps = torch.from_numpy(np.stack([layout.lens_at(s) for s in range(w.steps)])).to(dev)
+    torch.cuda.synchronize()
+    setup_s = time.perf_counter() - t_setup
+
+    attn = DecodeAttention(w.num_q_heads, w.num_kv_heads, B, layout.max_seq_len)
+    stream = torch.cuda.current_stream()
+
+    def step(s: int) -> None:
+        lens = lens_steps[s % w.steps]
+        for layer in range(w.layers):
+            attn.run(qs[layer], ks[layer % n_buf], vs[layer % n_buf], offsets, lens, w.scale,
+                     outs[layer], stream=stream)
+
+    for i in range(args.warmup):
+        step(i)
+    torch.cuda.synchronize()
+
+    graph = None
+    if args.graph:
+        graph = torch.cuda.CUDAGraph()
+        side = torch.cuda.Stream()
+        side.wait_stream(stream)
+        with torch.cuda.stream(side):
+            with torch.cuda.graph(graph, stream=side):
+                saved = stream
+                stream = side
+                for s in range(args.steps):
+                    step(s)
+                stream = saved
+        torch.cuda.synchronize()
+        graph.replay()  # warm replay
+        torch.cuda.synchronize()
+
+    start = torch.cuda.Event(enable_timing=True)
+    stop = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    start.record(stream)
+    if graph is not None:
+        graph.replay()
+    else:
+        for s in range(args.steps):
+            step(s)
+    stop.record(stream)
+    stop.synchronize()
+    torch.cuda.synchronize()
+    elapsed_s = start.elapsed_time(stop) / 1e3
+
+    step_bytes = [algorithmic_bytes(layout.lens_at(s % w.steps), w) * w.layers for s in range(args.steps)]
+    total_bytes = float(sum(step_bytes))
+    gbs = total_bytes / elapsed_s / 1e9
+    calls = args.steps * w.layers
+    call_s = elapsed_s / calls
+    per_call_bytes = total_bytes / calls
+    ms_per_step = elapsed_s * 1e3 / args.steps
+
+    if args.calibrate_copy_gib > 0:
+        n = int(args.calibrate_copy_gib * 2**30) // 4
+        src = torch.ones(n, dtype=torch.float32, device=dev)
+        dst = torch.empty_like(src)
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
+
+    result = {
+        "metric": METRIC,
+        "value": round(gbs, 2),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {
+            "workload": w.description,
+            "name": w.name,
+            "layers": w.layers,
+            "batch": B,
+            "num_q_heads": w.num_q_heads,
+            "num_kv_heads": w.num_kv_heads,
+            "head_dim": w.head_dim,
+            "decode_steps": w.steps,
+            "tokens_per_layer_step0": int(layout.lens.sum()),
+            "distinct_layer_buffers": n_buf,
+            "seed": wl.DEFAULT_SEED,
+            "launch": "hip_graph" if graph is not None else "stream",
+            "parallelism": "none (1 GPU)",
+        },
+        "frac_of_hbm_peak": round(gbs / HBM_PEAK_GBS, 4),
+        "decode_steps_per_s": round(args.steps / elapsed_s, 3),
+        "tokens_per_s": round(B * args.steps / elapsed_s, 1),
+        "roofline": {
+            "bound": "hbm",
+            "achieved": round(per_call_bytes / call_s / 1e9, 2),
+            "peak": HBM_PEAK_GBS,
+            "unit": "GB/s",
+            "frac": round(per_call_bytes / call_s / 1e9 / HBM_PEAK_GBS, 4),
+            "traffic": None,
+            "kernel": "one ctx_decode_attn_run call (decode_split_kernel + decode_merge_kernel)",
+            "bytes_per_launch": round(per_call_bytes),
+            "avg_launch_us": round(call_s * 1e6, 3),
+        },
+        "setup_s": round(setup_s, 1),
+    }
+    if not args.no_cpu_baseline:
+        threads = len(os.sched_getaffinity(0))
+        result["cpu_baseline"] = cpu_baseline(w, layout, args.cpu_seconds, threads)
+    print(json.dumps(result), flush=True)
+    attn.close()
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

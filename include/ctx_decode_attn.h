@@ -1,0 +1,128 @@
+/*
+ * ctx_decode_attn.h -- decode-step grouped-query attention over ragged
+ * per-sequence interaction-context KV caches, on one AMD Instinct MI355X
+ * (gfx950).
+ *
+ * Operation (one decode step of the student's rollout).  Every in-flight
+ * request b decodes one new token; its Hq query heads attend over the
+ * request's token context c_{t,j} = c_t + x_{t,<j} (Sec. 3, eq:token-context),
+ * whose keys and values are the request's cached rows.  For a
+ * reference-conditioned fast action the context is c_t + o^ref_{t+1}
+ * (Sec. 4.1, eq:reference-conditioned-action), for autonomous next-action
+ * prediction and for full responses it is c_t (eq:autonomous-action,
+ * eq:agent-response).  Requests run concurrently (the concurrency cap b_max of
+ * the rollout-efficiency study, tab:scheduling-hyperparameters), with tensor
+ * parallelism 1 so one GPU holds every head of a request, in bf16
+ * (tab:training-hyperparameters).  For every b < num_seqs and h < Hq:
+ *
+ *   g = Hq / Hkv,  kv = h / g              consecutive query heads share a KV head
+ *   r_t = seq_offsets[b] + t,  t < L_b = seq_lens[b]
+ *   s_t = scale * sum_d q[b,h,d] * k_cache[r_t,kv,d]
+ *   out[b,h,:] = sum_t softmax(s)_t * v_cache[r_t,kv,:]       (L_b = 0 -> zeros)
+ *
+ * Arithmetic: bf16 inputs, fp32 logits, fp32 softmax statistics and fp32
+ * accumulation.  The result matches the definition up to rounding
+ * (max-abs 1e-2 and mean-abs 1e-3 against a double-precision evaluation,
+ * typically ~1e-6).
+ *
+ * Conventions for every function below:
+ *  - All data pointers are DEVICE pointers on the handle's device unless
+ *    stated otherwise.  The caller owns them and keeps them alive until the
+ *    work queued on `stream` has completed.
+ *  - `stream` is a hipStream_t passed as void* (NULL = the default stream).
+ *  - Functions return a status code (ctx_status); nothing is thrown across
+ *    the ABI and nothing calls exit().  ctx_decode_attn_last_error() gives
+ *    a message for the last failing call on the calling thread.
+ */
+#ifndef CTX_DECODE_ATTN_H_
+#define CTX_DECODE_ATTN_H_
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  CTX_OK = 0,
+  CTX_ERR_INVALID_ARG = -1, /* NULL pointer, negative size, non-finite scale, bad desc field */
+  CTX_ERR_UNSUPPORTED = -2, /* head_dim != 128, Hq % Hkv != 0, group size Hq/Hkv > 16 */
+  CTX_ERR_CAPACITY = -3,    /* num_seqs > desc.max_batch */
+  CTX_ERR_ALIGNMENT = -4,   /* q, k_cache, v_cache or out not 16-byte aligned */
+  CTX_ERR_HIP = -5,         /* a HIP runtime or launch error (see ctx_decode_attn_last_error) */
+  CTX_ERR_OOM = -6          /* workspace allocation failed at create */
+} ctx_status;
+
+typedef enum { CTX_DTYPE_BF16 = 0, CTX_DTYPE_F32 = 1 } ctx_dtype;
+
+typedef struct ctx_decode_attn ctx_decode_attn; /* opaque handle */
+
+typedef struct {
+  int32_t num_q_heads;  /* Hq, the student's query heads (e.g. 16 or 32); Hq % Hkv == 0 */
+  int32_t num_kv_heads; /* Hkv, the shared KV heads (e.g. 8) */
+  int32_t head_dim;     /* D; only 128 is supported */
+  int32_t max_batch;    /* upper bound on num_seqs in any run call (sizes the workspace) */
+  int32_t max_seq_len;  /* upper bound on any seq_lens[b]; only sizes the workspace when
+                           split_tokens > 0 */
+  ctx_dtype out_dtype;  /* F32, or BF16 = round-to-nearest-even of the fp32 result */
+  int32_t split_tokens; /* 0: balanced split of the batch's tokens over the GPU (default);
+                           >= 16: every work range holds exactly this many tokens
+                           (tests use it to force split boundaries) */
+} ctx_decode_attn_desc;
+
+/*
+ * Create a handle on the current HIP device.  Validates desc, queries the
+ * device and allocates the fp32 split workspace (owned by the handle).
+ *   desc       host pointer, read only during the call
+ *   out_handle host pointer; receives the handle (NULL on failure)
+ * Errors: INVALID_ARG (NULL, non-positive sizes, split_tokens in 1..15, bad
+ * dtype), UNSUPPORTED (head_dim, head ratio), OOM, HIP.
+ */
+int ctx_decode_attn_create(const ctx_decode_attn_desc* desc, ctx_decode_attn** out_handle);
+
+/*
+ * Queue one decode-attention step on `stream`.  Asynchronous: no host
+ * synchronisation, no allocation and no host read of device data, so the
+ * call can be captured in a HIP graph.
+ *
+ *   q           bf16 [num_seqs, Hq, D], contiguous: the new token's queries
+ *   k_cache     bf16 [R, Hkv, D], contiguous rows: keys of every sequence
+ *   v_cache     bf16 [R, Hkv, D], same layout: values
+ *   seq_offsets int32 [num_seqs]: first cache row of sequence b
+ *   seq_lens    int32 [num_seqs]: rows attended by sequence b, the current
+ *               token included (its K/V row must already be in the cache)
+ *   num_seqs    number of sequences, 0 <= num_seqs <= desc.max_batch
+ *   scale       logit scale, e.g. 1/sqrt(128); applied in fp32 to q.k
+ *   out         [num_seqs, Hq, D] of desc.out_dtype, contiguous
+ *
+ * Sequence b reads rows [seq_offsets[b], seq_offsets[b] + seq_lens[b]); the
+ * regions may come in any order, may leave gaps between them (capacity
+ * reserved for growth), and must lie inside the cache.  seq_lens[b] = 0
+ * gives zeros.  Keys and values must be finite.  Device-side violations
+ * (regions outside the cache, seq_lens[b] < 0, seq_lens[b] > max_seq_len
+ * with split_tokens > 0) are undefined behaviour.
+ *
+ * The result is bitwise reproducible for fixed inputs on a fixed handle (no
+ * floating-point atomics).  One handle serves any number of sequential run
+ * calls on one stream (e.g. every layer); calls on different streams that
+ * may overlap need separate handles, because they share the workspace.
+ * Errors: INVALID_ARG, CAPACITY, ALIGNMENT, HIP.
+ */
+int ctx_decode_attn_run(ctx_decode_attn* handle, const void* q, const void* k_cache,
+                        const void* v_cache, const int32_t* seq_offsets, const int32_t* seq_lens,
+                        int32_t num_seqs, float scale, void* out, void* stream);
+
+/* Wait for the handle's device, free the workspace and the handle.  NULL is a no-op. */
+int ctx_decode_attn_destroy(ctx_decode_attn* handle);
+
+/* Static description of a status code (never NULL). */
+const char* ctx_decode_attn_status_string(int status);
+
+/* Message for the last failing call on the calling thread ("" if none). */
+const char* ctx_decode_attn_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* CTX_DECODE_ATTN_H_ */

@@ -11,7 +11,7 @@ import os
 
 import numpy as np
 
-from .build import LIB, build
+from . import build as _build
 
 _lib = None
 
@@ -19,9 +19,9 @@ _lib = None
 def _load():
     global _lib
     if _lib is None:
-        if not os.path.exists(LIB):
-            build()
-        lib = ctypes.CDLL(LIB)
+        if not os.path.exists(_build.LIB):
+            _build.build()
+        lib = ctypes.CDLL(_build.LIB)
         p, i32, i64, f64 = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_double
         lib.oracle_decode_attn.argtypes = [p, p, p, p, p, i32, i32, i32, i32, i64, f64, p, i32]
         lib.oracle_decode_attn.restype = ctypes.c_int

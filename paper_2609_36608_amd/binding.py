@@ -1,0 +1,169 @@
+"""ctypes binding of libctx_decode_attn.so: argument marshalling only.
+
+Every step of the attention runs in the library's HIP kernels; PyTorch only
+provides device memory and the stream.  There is no fallback: if the library
+is missing, loading fails with an error that says how to build it.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+from .build import LIB
+
+CTX_OK = 0
+CTX_ERR_INVALID_ARG = -1
+CTX_ERR_UNSUPPORTED = -2
+CTX_ERR_CAPACITY = -3
+CTX_ERR_ALIGNMENT = -4
+CTX_ERR_HIP = -5
+CTX_ERR_OOM = -6
+
+CTX_DTYPE_BF16 = 0
+CTX_DTYPE_F32 = 1
+
+# every function the C header declares
+EXPORTS = (
+    "ctx_decode_attn_create",
+    "ctx_decode_attn_run",
+    "ctx_decode_attn_destroy",
+    "ctx_decode_attn_status_string",
+    "ctx_decode_attn_last_error",
+)
+
+
+class CtxDesc(ctypes.Structure):
+    _fields_ = [
+        ("num_q_heads", ctypes.c_int32),
+        ("num_kv_heads", ctypes.c_int32),
+        ("head_dim", ctypes.c_int32),
+        ("max_batch", ctypes.c_int32),
+        ("max_seq_len", ctypes.c_int32),
+        ("out_dtype", ctypes.c_int),
+        ("split_tokens", ctypes.c_int32),
+    ]
+
+
+class CtxError(RuntimeError):
+    def __init__(self, status: int, message: str):
+        super().__init__(f"ctx_decode_attn status {status}: {message}")
+        self.status = status
+
+
+_lib = None
+
+
+def load_library(path: str | None = None):
+    """Load the HIP library (built in-tree by __graft_entry__.build())."""
+    global _lib
+    if _lib is not None and path is None:
+        return _lib
+    path = path or LIB
+    # torch ships its own libamdhip64.so.7; load it first so this library binds
+    # to the same HIP runtime as the streams and memory torch hands us
+    import torch  # noqa: F401
+
+    if not os.path.exists(path):
+        raise RuntimeError(f"{path} is missing: build it first (python -c 'import __graft_entry__ as g; g.build()')")
+    lib = ctypes.CDLL(path)
+    vp, i32 = ctypes.c_void_p, ctypes.c_int32
+    lib.ctx_decode_attn_create.argtypes = [ctypes.POINTER(CtxDesc), ctypes.POINTER(ctypes.c_void_p)]
+    lib.ctx_decode_attn_create.restype = ctypes.c_int
+    lib.ctx_decode_attn_run.argtypes = [vp, vp, vp, vp, vp, vp, i32, ctypes.c_float, vp, vp]
+    lib.ctx_decode_attn_run.restype = ctypes.c_int
+    lib.ctx_decode_attn_destroy.argtypes = [vp]
+    lib.ctx_decode_attn_destroy.restype = ctypes.c_int
+    lib.ctx_decode_attn_status_string.argtypes = [ctypes.c_int]
+    lib.ctx_decode_attn_status_string.restype = ctypes.c_char_p
+    lib.ctx_decode_attn_last_error.argtypes = []
+    lib.ctx_decode_attn_last_error.restype = ctypes.c_char_p
+    if path == LIB:
+        _lib = lib
+    return lib
+
+
+def error_for(lib, status: int) -> CtxError:
+    msg = lib.ctx_decode_attn_status_string(status).decode()
+    detail = lib.ctx_decode_attn_last_error().decode()
+    return CtxError(status, f"{msg}: {detail}" if detail else msg)
+
+
+def _dtype_code(dtype) -> int:
+    import torch
+
+    if dtype == torch.float32:
+        return CTX_DTYPE_F32
+    if dtype == torch.bfloat16:
+        return CTX_DTYPE_BF16
+    raise ValueError(f"out dtype must be float32 or bfloat16, not {dtype}")
+
+
+class DecodeAttention:
+    """Handle for ctx_decode_attn_run: decode-step GQA attention of one new token
+    per sequence over ragged KV caches [rows, Hkv, 128] (bf16)."""
+
+    def __init__(self, num_q_heads: int, num_kv_heads: int, max_batch: int, max_seq_len: int,
+                 head_dim: int = 128, out_dtype=None, split_tokens: int = 0):
+        import torch
+
+        self.lib = load_library()
+        self.out_dtype = torch.float32 if out_dtype is None else out_dtype
+        self.desc = CtxDesc(num_q_heads, num_kv_heads, head_dim, max_batch, max_seq_len,
+                            _dtype_code(self.out_dtype), split_tokens)
+        handle = ctypes.c_void_p()
+        rc = self.lib.ctx_decode_attn_create(ctypes.byref(self.desc), ctypes.byref(handle))
+        if rc != CTX_OK:
+            raise error_for(self.lib, rc)
+        self.handle = handle
+        self.device = torch.cuda.current_device()
+
+    def run(self, q, k_cache, v_cache, seq_offsets, seq_lens, scale: float, out, stream=None):
+        import torch
+
+        if self.handle is None:
+            raise RuntimeError("handle is closed")
+        d = self.desc
+        for name, t, dt in (("q", q, torch.bfloat16), ("k_cache", k_cache, torch.bfloat16),
+                            ("v_cache", v_cache, torch.bfloat16), ("seq_offsets", seq_offsets, torch.int32),
+                            ("seq_lens", seq_lens, torch.int32), ("out", out, self.out_dtype)):
+            if t.dtype != dt:
+                raise TypeError(f"{name} must be {dt}, got {t.dtype}")
+            if not t.is_cuda or t.device.index != self.device:
+                raise ValueError(f"{name} must be on cuda:{self.device}")
+            if not t.is_contiguous():
+                raise ValueError(f"{name} must be contiguous")
+        b = q.shape[0]
+        if q.shape != (b, d.num_q_heads, d.head_dim) or out.shape != q.shape:
+            raise ValueError(f"q/out must be [{b}, {d.num_q_heads}, {d.head_dim}]")
+        if k_cache.dim() != 3 or k_cache.shape[1:] != (d.num_kv_heads, d.head_dim) or v_cache.shape != k_cache.shape:
+            raise ValueError(f"k_cache/v_cache must be [rows, {d.num_kv_heads}, {d.head_dim}]")
+        if seq_offsets.shape != (b,) or seq_lens.shape != (b,):
+            raise ValueError(f"seq_offsets/seq_lens must be [{b}]")
+        if stream is None:
+            stream = torch.cuda.current_stream()
+        sp = stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream)
+        rc = self.lib.ctx_decode_attn_run(self.handle, q.data_ptr(), k_cache.data_ptr(), v_cache.data_ptr(),
+                                          seq_offsets.data_ptr(), seq_lens.data_ptr(), b, float(scale),
+                                          out.data_ptr(), sp)
+        if rc != CTX_OK:
+            raise error_for(self.lib, rc)
+        return out
+
+    def close(self):
+        if getattr(self, "handle", None) is not None:
+            rc = self.lib.ctx_decode_attn_destroy(self.handle)
+            self.handle = None
+            if rc != CTX_OK:
+                raise error_for(self.lib, rc)
+
+    def __enter__(self):
+        return self
+
+    def __exit__(self, *exc):
+        self.close()
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass

@@ -1,0 +1,728 @@
+// ctx_decode_attn.hip -- decode-step GQA attention over ragged KV caches for
+// gfx950 (MI355X), behind the C ABI declared in include/ctx_decode_attn.h.
+//
+// One decode step: every request's new token (Hq query heads) attends over the
+// request's token context c_{t,j} (Sec. 3, eq:token-context), i.e. its rows of
+// a shared [R, Hkv, D] bf16 cache; query head h reads KV head h / g.
+//
+// Design (flash-decoding split-K, register resident):
+//   * Work split.  The batch's tokens, flattened sequence after sequence, are
+//     cut into equal ranges, one range per group of Hkv single-wave
+//     workgroups (one wave per KV head), sized so the whole grid is resident
+//     at once.  Every wave derives its ranges from seq_lens on the device,
+//     so no host sync is needed and the call is graph-capturable.  A range
+//     that holds a whole sequence writes that sequence's output directly;
+//     otherwise each piece writes an fp32 partial (m, l, o) to the workspace
+//     and a second kernel merges the pieces of each (sequence, head).
+//   * Per 16-token block, all g query heads of the KV group are processed at
+//     once on the matrix cores:
+//       S^T[16 tok x 16]  = K_blk[16 x 128] . Q^T          4 x mfma 16x16x32 bf16
+//       V^T[16 dim x 16 tok] per 16 dims = V_blk . E_h      8 x mfma 16x16x32 bf16
+//         (E_h is a 0/1 selector; this transposes V exactly in registers)
+//       O^T[16 dim x 16]  += V^T . P^T                     8 x mfma 16x16x16 bf16,
+//         twice: P = P_hi + P_lo, both bf16, so P keeps ~16 mantissa bits.
+//     K and V are read from HBM exactly once, with 16-byte loads, straight
+//     into the MFMA operand registers; no LDS is used.
+//   * Online softmax in base 2 (scale * log2 e folded into the fp32 logits)
+//     with fp32 running max and sum.  The running max is raised only when a
+//     block's maximum exceeds it by more than 2^8, so probabilities stay
+//     <= 256 and the rescale of the accumulators is rare; the merge uses the
+//     same stale maxima, so the result is unchanged.
+//   * Merge: out = sum_s o_s 2^(m_s - M) / sum_s l_s 2^(m_s - M), M = max_s m_s,
+//     in fixed segment order (deterministic; no atomics).
+
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdarg>
+#include <cstdint>
+#include <cstdio>
+#include <cstring>
+#include <new>
+
+#include "ctx_decode_attn.h"
+
+namespace {
+
+constexpr int kHeadDim = 128;
+constexpr int kBlock = 16;        // tokens per MFMA block
+constexpr int kMaxGroup = 16;     // query heads per KV head (MFMA N dimension)
+constexpr int kMinRange = 64;     // smallest balanced range, tokens
+constexpr float kLazyRescale = 8.0f;  // log2 headroom before the running max moves
+constexpr int kMergeWaves = 4;
+constexpr int kXcds = 8;          // XCDs per MI355X; workgroups are dealt to them round-robin
+#ifndef CTX_WAVES_PER_EU
+#define CTX_WAVES_PER_EU 3
+#endif
+#ifndef CTX_ITER_BLOCKS
+#define CTX_ITER_BLOCKS 1
+#endif
+constexpr int kIterBlocks = CTX_ITER_BLOCKS;  // 16-token blocks loaded per loop trip
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+typedef short s16x4 __attribute__((ext_vector_type(4)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+typedef unsigned int u32x2 __attribute__((ext_vector_type(2)));
+
+struct Plan {
+  int32_t num_seqs;
+  int32_t hq;
+  int32_t hkv;
+  int32_t group;
+  int32_t num_ranges;    // ranges in the grid (each = hkv workgroups)
+  int32_t forced_width;  // > 0: fixed tokens per range
+  float scale_log2;      // scale * log2(e)
+};
+
+// ------------------------------------------------------------ wave helpers
+
+__device__ __forceinline__ int64_t wave_sum(int64_t x) {
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) x += __shfl_xor(x, off);
+  return x;
+}
+
+__device__ __forceinline__ float wave_max(float x) {
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) x = fmaxf(x, __shfl_xor(x, off));
+  return x;
+}
+
+// sum of lens[0 .. n)
+__device__ __forceinline__ int64_t sum_lens(const int32_t* __restrict__ lens, int n, int lane) {
+  int64_t acc = 0;
+  for (int i = lane; i < n; i += 64) acc += lens[i];
+  return wave_sum(acc);
+}
+
+// First sequence b whose flattened span [P_b, P_b + L_b) contains pos; *start = P_b.
+// Returns n if none.
+__device__ int find_sequence(const int32_t* __restrict__ lens, int n, int64_t pos, int lane,
+                             int64_t* start) {
+  int64_t carry = 0;
+  for (int base = 0; base < n; base += 64) {
+    const int i = base + lane;
+    const int64_t len = i < n ? lens[i] : 0;
+    int64_t incl = len;
+#pragma unroll
+    for (int off = 1; off < 64; off <<= 1) {
+      const int64_t y = __shfl_up(incl, off);
+      if (lane >= off) incl += y;
+    }
+    const int64_t excl = incl - len;
+    const unsigned long long hit = __ballot(carry + excl <= pos && pos < carry + incl);
+    if (hit) {
+      const int src = __ffsll(hit) - 1;
+      *start = __shfl(carry + excl, src);
+      return base + src;
+    }
+    carry += __shfl(incl, 63);
+  }
+  *start = carry;
+  return n;
+}
+
+__device__ __forceinline__ int64_t range_width(int64_t total, const Plan& p) {
+  if (p.forced_width > 0) return p.forced_width;
+  int64_t w = (total + p.num_ranges - 1) / p.num_ranges;
+  w = (w + kBlock - 1) / kBlock * kBlock;
+  return w < kMinRange ? kMinRange : w;
+}
+
+// ------------------------------------------------------------ math helpers
+
+__device__ __forceinline__ bf16x8 as_bf16x8(u32x4 v) { return __builtin_bit_cast(bf16x8, v); }
+
+__device__ __forceinline__ uint32_t pack_bf16x2(float a, float b) {
+  bf16x2 v = {(__bf16)a, (__bf16)b};  // round to nearest even
+  return __builtin_bit_cast(uint32_t, v);
+}
+
+__device__ __forceinline__ s16x4 pack_bf16x4(float a, float b, float c, float d) {
+  u32x2 u = {pack_bf16x2(a, b), pack_bf16x2(c, d)};
+  return __builtin_bit_cast(s16x4, u);
+}
+
+__device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
+
+#ifndef CTX_LDS_STAGE
+#define CTX_LDS_STAGE 1
+#endif
+#ifndef CTX_NT_LOADS
+#define CTX_NT_LOADS CTX_LDS_STAGE
+#endif
+#ifndef CTX_PREFETCH
+#define CTX_PREFETCH 0
+#endif
+
+__device__ __forceinline__ u32x4 load16(const uint16_t* p) {
+#if CTX_NT_LOADS
+  return __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(p));
+#else
+  return *reinterpret_cast<const u32x4*>(p);
+#endif
+}
+
+// Buffer resources: a wave-uniform base and byte size; loads past the size
+// return zeros, which covers the ragged last block of a segment.
+constexpr int kRsrcWord3 = 0x00020000;  // raw buffer, 32-bit data format
+constexpr int kLoadAux = CTX_NT_LOADS ? 2 : 0;  // 2 = non-temporal (streamed once)
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const uint16_t* base, uint32_t bytes) {
+  const uint64_t a = reinterpret_cast<uint64_t>(base);
+  const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)a);
+  const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(a >> 32));
+  const uint64_t u = ((uint64_t)hi << 32) | lo;
+  return __builtin_amdgcn_make_buffer_rsrc(reinterpret_cast<void*>(u), (short)0,
+                                           (int)__builtin_amdgcn_readfirstlane(bytes), kRsrcWord3);
+}
+
+__device__ __forceinline__ u32x4 buf_load16(__amdgpu_buffer_rsrc_t r, int voff, int soff) {
+  return __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, kLoadAux));
+}
+
+// One lane's share of a 16-token block of one KV head: token `tok` (relative
+// to the segment), the 4 x 16-byte pieces at dims 32*kk + 8*c .. +8.
+// `base` already points at dim 8*c of the segment's first row for this head.
+template <bool kPred>
+__device__ __forceinline__ void load_block(u32x4 (&r)[4], const uint16_t* __restrict__ base,
+                                           size_t row_elems, int tok, int len) {
+  if (!kPred || tok < len) {
+    const uint16_t* ptr = base + (size_t)tok * row_elems;
+#pragma unroll
+    for (int kk = 0; kk < 4; ++kk) r[kk] = load16(ptr + 32 * kk);
+  } else {
+#pragma unroll
+    for (int kk = 0; kk < 4; ++kk) r[kk] = u32x4{0u, 0u, 0u, 0u};
+  }
+}
+
+// Coalesced share of a 16-token block: lane l loads 16 bytes (chunk l % 16) of
+// tokens tok, tok + 4, tok + 8, tok + 12 (tok = l / 16 + block start).
+// `base` already points at the lane's chunk of the segment's first row.
+template <bool kPred>
+__device__ __forceinline__ void load_coalesced(u32x4 (&r)[4], const uint16_t* __restrict__ base,
+                                               size_t row_elems, int tok, int len) {
+#pragma unroll
+  for (int u = 0; u < 4; ++u) {
+    const int t = tok + 4 * u;
+    if (!kPred || t < len)
+      r[u] = load16(base + (size_t)t * row_elems);
+    else
+      r[u] = u32x4{0u, 0u, 0u, 0u};
+  }
+}
+
+// Softmax state of one lane: query head n of the group (lanes with n >= g
+// carry unused columns), for the 4 tokens 4c..4c+3 of each block.
+struct Softmax {
+  float m;  // running max (log2 units), uniform over the 4 lanes of a query
+  float l;  // this lane's share of the running sum
+};
+
+// Process one 16-token block.  `valid` = tokens of the block inside the segment.
+__device__ __forceinline__ void attend_block(const u32x4 (&kr)[4], const u32x4 (&vr)[4],
+                                             const bf16x8 (&qb)[4], const bf16x8 (&sel)[2],
+                                             int valid, int c, float scale_log2, Softmax& st,
+                                             f32x4 (&o)[8]) {
+  // logits: lane (c, n) gets tokens 4c+i, query n
+  f32x4 s = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int kk = 0; kk < 4; ++kk)
+    s = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(kr[kk]), qb[kk], s, 0, 0, 0);
+
+  float x[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    x[i] = s[i] * scale_log2;
+    if (4 * c + i >= valid) x[i] = -INFINITY;
+  }
+  float mx = fmaxf(fmaxf(x[0], x[1]), fmaxf(x[2], x[3]));
+  mx = fmaxf(mx, __shfl_xor(mx, 16));
+  mx = fmaxf(mx, __shfl_xor(mx, 32));
+  if (__any(mx > st.m + kLazyRescale)) {
+    const float m_new = fmaxf(st.m, mx);
+    const float alpha = fast_exp2(st.m - m_new);  // 0 on the first block (m = -inf)
+    st.l *= alpha;
+#pragma unroll
+    for (int nb = 0; nb < 8; ++nb) o[nb] *= alpha;
+    st.m = m_new;
+  }
+  float p[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) p[i] = fast_exp2(x[i] - st.m);
+  st.l += (p[0] + p[1]) + (p[2] + p[3]);
+
+  // P as the B operand of a 16x16x16 MFMA: slot (c, j) = token 4c + j.
+  // Split into hi + lo bf16 parts.
+  float hi[4], lo[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    hi[i] = (float)(__bf16)p[i];
+    lo[i] = p[i] - hi[i];
+  }
+  const s16x4 p_hi = pack_bf16x4(hi[0], hi[1], hi[2], hi[3]);
+  const s16x4 p_lo = pack_bf16x4(lo[0], lo[1], lo[2], lo[3]);
+
+  const f32x4 zero = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int kk = 0; kk < 4; ++kk) {
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      // lane (c, n): V[token 4c+i][dim 32kk + 16h + n], exact
+      const f32x4 t = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(vr[kk]), sel[h], zero, 0, 0, 0);
+      const s16x4 vt = pack_bf16x4(t[0], t[1], t[2], t[3]);
+      const int nb = 2 * kk + h;
+      o[nb] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(vt, p_hi, o[nb], 0, 0, 0);
+      o[nb] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(vt, p_lo, o[nb], 0, 0, 0);
+    }
+  }
+}
+
+template <typename OutT>
+__device__ __forceinline__ void store4(OutT* dst, f32x4 v);
+
+template <>
+__device__ __forceinline__ void store4<float>(float* dst, f32x4 v) {
+  *reinterpret_cast<f32x4*>(dst) = v;
+}
+
+template <>
+__device__ __forceinline__ void store4<uint16_t>(uint16_t* dst, f32x4 v) {
+  u32x2 u = {pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3])};
+  *reinterpret_cast<u32x2*>(dst) = u;
+}
+
+template <typename OutT>
+__device__ __forceinline__ void store2(OutT* dst, float a, float b);
+
+template <>
+__device__ __forceinline__ void store2<float>(float* dst, float a, float b) {
+  *reinterpret_cast<float2*>(dst) = make_float2(a, b);
+}
+
+template <>
+__device__ __forceinline__ void store2<uint16_t>(uint16_t* dst, float a, float b) {
+  *reinterpret_cast<uint32_t*>(dst) = pack_bf16x2(a, b);
+}
+
+// ------------------------------------------------------------ split kernel
+
+template <typename OutT>
+__global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(CTX_WAVES_PER_EU))) void decode_split_kernel(
+    const uint16_t* __restrict__ q, const uint16_t* __restrict__ kc,
+    const uint16_t* __restrict__ vc, const int32_t* __restrict__ offs,
+    const int32_t* __restrict__ lens, Plan p, float* __restrict__ o_ws,
+    float2* __restrict__ ml_ws, OutT* __restrict__ out) {
+  const int lane = threadIdx.x;
+  const int n = lane & 15;
+  const int c = lane >> 4;
+  // Workgroups are dealt round-robin over the XCDs (id % kXcds).  Give all KV
+  // heads of a range the same XCD, so each XCD streams whole cache rows
+  // (every head of a token) through its own L2.  num_ranges % kXcds == 0.
+  const int xcd = blockIdx.x % kXcds;
+  const int idx = blockIdx.x / kXcds;
+  const int kv = idx % p.hkv;
+  const int w = (idx / p.hkv) * kXcds + xcd;
+  const int g = p.group;
+#if CTX_LDS_STAGE
+  __shared__ __attribute__((aligned(16))) uint16_t lds_k[kBlock * kHeadDim];
+  __shared__ __attribute__((aligned(16))) uint16_t lds_v[kBlock * kHeadDim];
+#endif
+
+  const int64_t total = sum_lens(lens, p.num_seqs, lane);
+  const int64_t width = range_width(total, p);
+  const int64_t ws = (int64_t)w * width;
+  if (ws >= total) return;
+  const int64_t we = ws + width < total ? ws + width : total;
+
+  // selectors E_h: lane (c, n), slot j is 1 iff dim 8c + j == 16h + n
+  bf16x8 sel[2];
+#pragma unroll
+  for (int h = 0; h < 2; ++h)
+#pragma unroll
+    for (int j = 0; j < 8; ++j) sel[h][j] = (8 * c + j == 16 * h + n) ? (__bf16)1.0f : (__bf16)0.0f;
+
+  const size_t row_elems = (size_t)p.hkv * kHeadDim;
+  int64_t pos;
+  int b = find_sequence(lens, p.num_seqs, ws, lane, &pos);
+  while (b < p.num_seqs && pos < we) {
+    const int seq_len = lens[b];
+    const int64_t s0 = ws > pos ? ws - pos : 0;
+    const int64_t s1 = we - pos < seq_len ? we - pos : seq_len;
+    if (s1 > s0) {
+      const int len = (int)(s1 - s0);
+      bf16x8 qb[4];
+      if (n < g) {
+        const uint16_t* qrow = q + ((size_t)b * p.hq + (size_t)kv * g + n) * kHeadDim + 8 * c;
+#pragma unroll
+        for (int kk = 0; kk < 4; ++kk) qb[kk] = as_bf16x8(load16(qrow + 32 * kk));
+      } else {
+#pragma unroll
+        for (int kk = 0; kk < 4; ++kk) qb[kk] = as_bf16x8(u32x4{0u, 0u, 0u, 0u});
+      }
+      Softmax st{-INFINITY, 0.f};
+      f32x4 o[8];
+#pragma unroll
+      for (int nb = 0; nb < 8; ++nb) o[nb] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+      const uint16_t* kseg = kc + ((size_t)offs[b] + (size_t)s0) * row_elems + (size_t)kv * kHeadDim;
+      const uint16_t* vseg = vc + ((size_t)offs[b] + (size_t)s0) * row_elems + (size_t)kv * kHeadDim;
+      const int row_bytes = (int)(row_elems * 2);
+      const size_t blk_elems = (size_t)kBlock * row_elems;
+#if CTX_LDS_STAGE
+      // Coalesced loads: 16 lanes cover one token's 256-byte head slice, four
+      // tokens per instruction.  The block goes through a wave-private LDS
+      // tile (16-byte chunks XOR-swizzled by token, conflict-free both ways)
+      // and is read back in the MFMA operand layout.
+      const int voff = (lane >> 4) * row_bytes + (lane & 15) * 16;
+      const int ld_tok = lane >> 4;
+      for (int t = 0; t < len; t += kBlock) {
+        const uint32_t bytes = (uint32_t)((len - t < kBlock ? len - t : kBlock) * row_bytes);
+        const __amdgpu_buffer_rsrc_t rk = make_rsrc(kseg + (size_t)(t / kBlock) * blk_elems, bytes);
+        const __amdgpu_buffer_rsrc_t rv = make_rsrc(vseg + (size_t)(t / kBlock) * blk_elems, bytes);
+        u32x4 pk[4], pv[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          pk[u] = buf_load16(rk, voff, 4 * u * row_bytes);
+          pv[u] = buf_load16(rv, voff, 4 * u * row_bytes);
+        }
+        __syncthreads();  // previous block's LDS reads are done
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          const int tok = 4 * u + ld_tok;
+          const int slot = tok * kHeadDim + (((lane & 15) ^ tok) << 3);
+          *reinterpret_cast<u32x4*>(&lds_k[slot]) = pk[u];
+          *reinterpret_cast<u32x4*>(&lds_v[slot]) = pv[u];
+        }
+        __syncthreads();
+        u32x4 kr[4], vr[4];
+#pragma unroll
+        for (int kk = 0; kk < 4; ++kk) {
+          const int slot = n * kHeadDim + (((4 * kk + c) ^ n) << 3);
+          kr[kk] = *reinterpret_cast<const u32x4*>(&lds_k[slot]);
+          vr[kk] = *reinterpret_cast<const u32x4*>(&lds_v[slot]);
+        }
+        attend_block(kr, vr, qb, sel, len - t < kBlock ? len - t : kBlock, c, p.scale_log2, st, o);
+      }
+#else
+      // Loads straight into the MFMA operand layout: lane (c, n) reads token n,
+      // bytes 64*kk + 16*c of the head slice.
+      const int voff = n * row_bytes + c * 16;
+      for (int t = 0; t < len; t += kIterBlocks * kBlock) {
+        u32x4 kr[kIterBlocks][4], vr[kIterBlocks][4];
+#pragma unroll
+        for (int i = 0; i < kIterBlocks; ++i) {
+          const int tb = t + i * kBlock;
+          const int rem = len - tb;
+          const uint32_t bytes = (uint32_t)((rem <= 0 ? 0 : rem < kBlock ? rem : kBlock) * row_bytes);
+          const __amdgpu_buffer_rsrc_t rk = make_rsrc(kseg + (size_t)(tb / kBlock) * blk_elems, bytes);
+          const __amdgpu_buffer_rsrc_t rv = make_rsrc(vseg + (size_t)(tb / kBlock) * blk_elems, bytes);
+#pragma unroll
+          for (int kk = 0; kk < 4; ++kk) {
+            kr[i][kk] = buf_load16(rk, voff + 64 * kk, 0);
+            vr[i][kk] = buf_load16(rv, voff + 64 * kk, 0);
+          }
+        }
+#pragma unroll
+        for (int i = 0; i < kIterBlocks; ++i) {
+          const int rem = len - (t + i * kBlock);
+          if (rem > 0) attend_block(kr[i], vr[i], qb, sel, rem < kBlock ? rem : kBlock, c, p.scale_log2, st, o);
+        }
+      }
+#endif
+
+      float l_tot = st.l + __shfl_xor(st.l, 16);
+      l_tot += __shfl_xor(l_tot, 32);
+      if (s0 == 0 && s1 == seq_len) {
+        // the whole sequence is in this range: final output
+        if (n < g) {
+          const float inv = 1.0f / l_tot;
+          OutT* orow = out + ((size_t)b * p.hq + (size_t)kv * g + n) * kHeadDim + 4 * c;
+#pragma unroll
+          for (int nb = 0; nb < 8; ++nb) store4<OutT>(orow + 16 * nb, o[nb] * inv);
+        }
+      } else {
+        const size_t idx = ((size_t)(w + b) * p.hkv + kv) * g + n;
+        if (n < g) {
+          float* orow = o_ws + idx * kHeadDim + 4 * c;
+#pragma unroll
+          for (int nb = 0; nb < 8; ++nb) *reinterpret_cast<f32x4*>(orow + 16 * nb) = o[nb];
+          if (c == 0) ml_ws[idx] = make_float2(st.m, l_tot);
+        }
+      }
+    }
+    pos += seq_len;
+    ++b;
+  }
+}
+
+// ------------------------------------------------------------ merge kernel
+
+__device__ __forceinline__ float lane_value(float x, int src) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, x), src));
+}
+
+// One wave per (sequence, query head); lane l owns dims 2l, 2l+1.  Segment
+// weights are computed one segment per lane; the partial outputs are then
+// read eight segments at a time so their loads overlap.
+template <typename OutT>
+__global__ __launch_bounds__(64 * kMergeWaves) void decode_merge_kernel(
+    const int32_t* __restrict__ lens, Plan p, const float* __restrict__ o_ws,
+    const float2* __restrict__ ml_ws, OutT* __restrict__ out) {
+  const int lane = threadIdx.x & 63;
+  const int gw = blockIdx.x * kMergeWaves + (threadIdx.x >> 6);
+  if (gw >= p.num_seqs * p.hq) return;
+  const int b = gw / p.hq;
+  const int h = gw - b * p.hq;
+  const int kv = h / p.group;
+  const int qi = h - kv * p.group;
+  const int seq_len = lens[b];
+  float r0 = 0.f, r1 = 0.f;
+  if (seq_len > 0) {
+    const int64_t total = sum_lens(lens, p.num_seqs, lane);
+    const int64_t pos = sum_lens(lens, b, lane);
+    const int64_t width = range_width(total, p);
+    const int64_t wf = pos / width;
+    int64_t wl = (pos + seq_len - 1) / width;
+    if (wf == wl) return;  // written by the split kernel
+    // only reachable when seq_lens breaks the max_seq_len contract: stay in the workspace
+    if (wl >= p.num_ranges) wl = p.num_ranges - 1;
+    const int nseg = (int)(wl - wf + 1);
+    // partial (m, l, o) of segment j lives at slot wf + j + b
+    const size_t first = ((size_t)(wf + b) * p.hkv + kv) * p.group + qi;
+    const size_t stride = (size_t)p.hkv * p.group;
+    float m = -INFINITY;
+    for (int j = lane; j < nseg; j += 64) m = fmaxf(m, ml_ws[first + j * stride].x);
+    m = wave_max(m);
+    float lsum = 0.f;
+    for (int base = 0; base < nseg; base += 64) {
+      const int j = base + lane;
+      float wj = 0.f;
+      if (j < nseg) {
+        const float2 ml = ml_ws[first + j * stride];
+        wj = fast_exp2(ml.x - m);
+        lsum += wj * ml.y;
+      }
+      const int cnt = nseg - base < 64 ? nseg - base : 64;
+      for (int s0 = 0; s0 < cnt; s0 += 8) {
+        float2 ov[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u)
+          ov[u] = s0 + u < cnt
+                      ? reinterpret_cast<const float2*>(
+                            o_ws + (first + (size_t)(base + s0 + u) * stride) * kHeadDim)[lane]
+                      : make_float2(0.f, 0.f);
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+          const float wgt = lane_value(wj, (s0 + u) & 63);
+          r0 += wgt * ov[u].x;
+          r1 += wgt * ov[u].y;
+        }
+      }
+    }
+    for (int off = 32; off > 0; off >>= 1) lsum += __shfl_xor(lsum, off);
+    const float inv = 1.0f / lsum;
+    r0 *= inv;
+    r1 *= inv;
+  }
+  store2<OutT>(out + ((size_t)b * p.hq + h) * kHeadDim + 2 * lane, r0, r1);
+}
+
+// ------------------------------------------------------------ host side
+
+thread_local char g_last_error[512] = "";
+
+int fail(int code, const char* fmt, ...) {
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(g_last_error, sizeof g_last_error, fmt, ap);
+  va_end(ap);
+  return code;
+}
+
+int hip_fail(hipError_t e, const char* what) {
+  return fail(CTX_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+bool aligned16(const void* ptr) { return (reinterpret_cast<uintptr_t>(ptr) & 15u) == 0; }
+
+int64_t round_up(int64_t x, int64_t m) { return (x + m - 1) / m * m; }
+
+}  // namespace
+
+struct ctx_decode_attn {
+  ctx_decode_attn_desc desc;
+  int device;
+  int num_cus;
+  int32_t ranges_auto;  // ranges of the balanced split
+  int64_t max_ranges;   // most ranges any run call can use
+  float* o_ws;
+  float2* ml_ws;
+};
+
+extern "C" {
+
+const char* ctx_decode_attn_status_string(int status) {
+  switch (status) {
+    case CTX_OK: return "ok";
+    case CTX_ERR_INVALID_ARG: return "invalid argument";
+    case CTX_ERR_UNSUPPORTED: return "unsupported shape";
+    case CTX_ERR_CAPACITY: return "num_seqs exceeds max_batch";
+    case CTX_ERR_ALIGNMENT: return "pointer not 16-byte aligned";
+    case CTX_ERR_HIP: return "HIP runtime error";
+    case CTX_ERR_OOM: return "out of device memory";
+    default: return "unknown status";
+  }
+}
+
+const char* ctx_decode_attn_last_error(void) { return g_last_error; }
+
+int ctx_decode_attn_create(const ctx_decode_attn_desc* desc, ctx_decode_attn** out_handle) {
+  g_last_error[0] = '\0';
+  if (out_handle == nullptr) return fail(CTX_ERR_INVALID_ARG, "out_handle is NULL");
+  *out_handle = nullptr;
+  if (desc == nullptr) return fail(CTX_ERR_INVALID_ARG, "desc is NULL");
+  const ctx_decode_attn_desc d = *desc;
+  if (d.num_q_heads <= 0 || d.num_kv_heads <= 0)
+    return fail(CTX_ERR_INVALID_ARG, "head counts must be positive (Hq=%d, Hkv=%d)",
+                d.num_q_heads, d.num_kv_heads);
+  if (d.head_dim != kHeadDim)
+    return fail(CTX_ERR_UNSUPPORTED, "head_dim %d unsupported (only %d)", d.head_dim, kHeadDim);
+  if (d.num_q_heads % d.num_kv_heads != 0)
+    return fail(CTX_ERR_UNSUPPORTED, "Hq=%d is not a multiple of Hkv=%d", d.num_q_heads,
+                d.num_kv_heads);
+  if (d.num_q_heads / d.num_kv_heads > kMaxGroup)
+    return fail(CTX_ERR_UNSUPPORTED, "group size %d > %d", d.num_q_heads / d.num_kv_heads,
+                kMaxGroup);
+  if (d.max_batch <= 0 || d.max_seq_len <= 0)
+    return fail(CTX_ERR_INVALID_ARG, "max_batch and max_seq_len must be positive");
+  if (d.out_dtype != CTX_DTYPE_BF16 && d.out_dtype != CTX_DTYPE_F32)
+    return fail(CTX_ERR_INVALID_ARG, "unknown out_dtype %d", (int)d.out_dtype);
+  if (d.split_tokens < 0 || (d.split_tokens > 0 && d.split_tokens < kBlock))
+    return fail(CTX_ERR_INVALID_ARG, "split_tokens must be 0 or >= %d", kBlock);
+
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+  int cus = 0;
+  e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
+  if (e != hipSuccess) return hip_fail(e, "hipDeviceGetAttribute");
+  int per_cu = 0;
+  if (d.out_dtype == CTX_DTYPE_F32)
+    e = hipOccupancyMaxActiveBlocksPerMultiprocessor(
+        &per_cu, reinterpret_cast<const void*>(&decode_split_kernel<float>), 64, 0);
+  else
+    e = hipOccupancyMaxActiveBlocksPerMultiprocessor(
+        &per_cu, reinterpret_cast<const void*>(&decode_split_kernel<uint16_t>), 64, 0);
+  if (e != hipSuccess) return hip_fail(e, "hipOccupancyMaxActiveBlocksPerMultiprocessor");
+  if (per_cu < 1) per_cu = 1;
+
+  // one resident wave per (range, KV head); ranges in whole multiples of the XCD count
+  int64_t ranges_auto = (int64_t)cus * per_cu / d.num_kv_heads / kXcds * kXcds;
+  if (ranges_auto < kXcds) ranges_auto = kXcds;
+  int64_t max_ranges = ranges_auto;
+  if (d.split_tokens > 0)
+    max_ranges = round_up(((int64_t)d.max_batch * d.max_seq_len + d.split_tokens - 1) / d.split_tokens, kXcds);
+  if (max_ranges * d.num_kv_heads > INT32_MAX)
+    return fail(CTX_ERR_INVALID_ARG, "split_tokens %d too small for max_batch x max_seq_len",
+                d.split_tokens);
+
+  const int64_t slots = max_ranges + d.max_batch;
+  const size_t o_bytes = (size_t)slots * d.num_q_heads * kHeadDim * sizeof(float);
+  const size_t ml_bytes = (size_t)slots * d.num_q_heads * sizeof(float2);
+
+  ctx_decode_attn* h = new (std::nothrow) ctx_decode_attn{};
+  if (h == nullptr) return fail(CTX_ERR_OOM, "host allocation failed");
+  h->desc = d;
+  h->device = dev;
+  h->num_cus = cus;
+  h->ranges_auto = (int32_t)ranges_auto;
+  h->max_ranges = max_ranges;
+  e = hipMalloc(reinterpret_cast<void**>(&h->o_ws), o_bytes);
+  if (e == hipSuccess) e = hipMalloc(reinterpret_cast<void**>(&h->ml_ws), ml_bytes);
+  if (e != hipSuccess) {
+    (void)hipGetLastError();
+    if (h->o_ws) (void)hipFree(h->o_ws);
+    delete h;
+    return fail(CTX_ERR_OOM, "workspace of %zu bytes: %s", o_bytes + ml_bytes, hipGetErrorString(e));
+  }
+  *out_handle = h;
+  return CTX_OK;
+}
+
+int ctx_decode_attn_run(ctx_decode_attn* h, const void* q, const void* k_cache,
+                        const void* v_cache, const int32_t* seq_offsets, const int32_t* seq_lens,
+                        int32_t num_seqs, float scale, void* out, void* stream) {
+  if (h == nullptr) return fail(CTX_ERR_INVALID_ARG, "handle is NULL");
+  if (num_seqs < 0) return fail(CTX_ERR_INVALID_ARG, "num_seqs %d < 0", num_seqs);
+  if (num_seqs > h->desc.max_batch)
+    return fail(CTX_ERR_CAPACITY, "num_seqs %d > max_batch %d", num_seqs, h->desc.max_batch);
+  if (!std::isfinite(scale)) return fail(CTX_ERR_INVALID_ARG, "scale is not finite");
+  if (num_seqs == 0) return CTX_OK;
+  if (q == nullptr || k_cache == nullptr || v_cache == nullptr || seq_offsets == nullptr ||
+      seq_lens == nullptr || out == nullptr)
+    return fail(CTX_ERR_INVALID_ARG, "NULL data pointer");
+  if (!aligned16(q) || !aligned16(k_cache) || !aligned16(v_cache) || !aligned16(out))
+    return fail(CTX_ERR_ALIGNMENT, "q, k_cache, v_cache and out must be 16-byte aligned");
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+  if (dev != h->device)
+    return fail(CTX_ERR_INVALID_ARG, "current device %d is not the handle's device %d", dev,
+                h->device);
+
+  const ctx_decode_attn_desc& d = h->desc;
+  Plan p;
+  p.num_seqs = num_seqs;
+  p.hq = d.num_q_heads;
+  p.hkv = d.num_kv_heads;
+  p.group = d.num_q_heads / d.num_kv_heads;
+  p.forced_width = d.split_tokens;
+  p.num_ranges = d.split_tokens > 0
+                     ? (int32_t)round_up(((int64_t)num_seqs * d.max_seq_len + d.split_tokens - 1) /
+                                             d.split_tokens, kXcds)
+                     : h->ranges_auto;
+  p.scale_log2 = (float)((double)scale * 1.4426950408889634);
+
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  const dim3 split_grid((unsigned)(p.num_ranges * p.hkv));
+  const dim3 merge_grid((unsigned)(((int64_t)num_seqs * p.hq + kMergeWaves - 1) / kMergeWaves));
+  const uint16_t* qp = static_cast<const uint16_t*>(q);
+  const uint16_t* kp = static_cast<const uint16_t*>(k_cache);
+  const uint16_t* vp = static_cast<const uint16_t*>(v_cache);
+  if (d.out_dtype == CTX_DTYPE_F32) {
+    float* op = static_cast<float*>(out);
+    hipLaunchKernelGGL(decode_split_kernel<float>, split_grid, dim3(64), 0, s, qp, kp, vp,
+                       seq_offsets, seq_lens, p, h->o_ws, h->ml_ws, op);
+    hipLaunchKernelGGL(decode_merge_kernel<float>, merge_grid, dim3(64 * kMergeWaves), 0, s,
+                       seq_lens, p, h->o_ws, h->ml_ws, op);
+  } else {
+    uint16_t* op = static_cast<uint16_t*>(out);
+    hipLaunchKernelGGL(decode_split_kernel<uint16_t>, split_grid, dim3(64), 0, s, qp, kp, vp,
+                       seq_offsets, seq_lens, p, h->o_ws, h->ml_ws, op);
+    hipLaunchKernelGGL(decode_merge_kernel<uint16_t>, merge_grid, dim3(64 * kMergeWaves), 0, s,
+                       seq_lens, p, h->o_ws, h->ml_ws, op);
+  }
+  e = hipGetLastError();
+  if (e != hipSuccess) return hip_fail(e, "kernel launch");
+  return CTX_OK;
+}
+
+int ctx_decode_attn_destroy(ctx_decode_attn* h) {
+  if (h == nullptr) return CTX_OK;
+  int rc = CTX_OK;
+  int prev = -1;
+  if (hipGetDevice(&prev) == hipSuccess && prev != h->device) (void)hipSetDevice(h->device);
+  hipError_t e = hipDeviceSynchronize();
+  if (e != hipSuccess) rc = hip_fail(e, "hipDeviceSynchronize");
+  if (h->o_ws) (void)hipFree(h->o_ws);
+  if (h->ml_ws) (void)hipFree(h->ml_ws);
+  if (prev >= 0 && prev != h->device) (void)hipSetDevice(prev);
+  delete h;
+  return rc;
+}
+
+}  // extern "C"
