@@ -319,13 +319,13 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(CTX_WAVES_PE
   const int lane = threadIdx.x;
   const int n = lane & 15;
   const int c = lane >> 4;
-  // Workgroups are dealt round-robin over the XCDs (id % kXcds).  Give all KV
-  // heads of a range the same XCD, so each XCD streams whole cache rows
-  // (every head of a token) through its own L2.  num_ranges % kXcds == 0.
-  const int xcd = blockIdx.x % kXcds;
-  const int idx = blockIdx.x / kXcds;
-  const int kv = idx % p.hkv;
-  const int w = (idx / p.hkv) * kXcds + xcd;
+  // Range-major order: consecutive workgroups take consecutive ranges of one
+  // KV head.  Workgroups are dealt round-robin over the XCDs (id % kXcds) and
+  // num_ranges % kXcds == 0, so every head of a range lands on the same XCD
+  // (range w on XCD w % kXcds) while each CU holds the same head of nearby
+  // ranges.  Measured on MI355X this order streams the cache fastest.
+  const int kv = blockIdx.x / p.num_ranges;
+  const int w = blockIdx.x - kv * p.num_ranges;
   const int g = p.group;
 #if CTX_LDS_STAGE
   __shared__ __attribute__((aligned(16))) uint16_t lds_k[kBlock * kHeadDim];
