@@ -38,6 +38,29 @@ def algorithmic_bytes(lens: np.ndarray, w: wl.Workload, out_bytes: int = 4) -> i
     return kv + b * w.num_q_heads * w.head_dim * (2 + out_bytes) + 8 * b
 
 
+def profiled_traffic(workload: str):
+    """HBM bytes per split-kernel launch from the committed rocprofv3 counter
+    summary, or None if that summary is for another workload or for an older
+    version of the kernel source."""
+    import glob
+    import hashlib
+
+    src = os.path.join(ROOT, "paper_2609_36608_amd", "csrc", "ctx_decode_attn.hip")
+    digest = hashlib.sha256(open(src, "rb").read()).hexdigest()
+    for path in glob.glob(os.path.join(ROOT, "profiles", "*hbm_traffic*.md")):
+        fields = {}
+        for line in open(path):
+            if ":" in line and not line.startswith(("|", "#", "`")):
+                k, _, v = line.partition(":")
+                fields[k.strip()] = v.strip()
+        if fields.get("kernel_source_sha256") == digest and fields.get("workload") == workload:
+            t = int(fields["traffic_bytes_per_launch"])
+            a = int(fields["algorithmic_bytes_per_launch"])
+            return {"bytes_per_launch": t, "ratio_to_algorithmic": round(t / a, 4),
+                    "source": os.path.relpath(path, ROOT)}
+    return None
+
+
 def cpu_baseline(w: wl.Workload, layout: wl.Layout, target_s: float, threads: int) -> dict:
     """Time the CPU oracle on layer 0 / step 0 for a fixed sample of sequences,
     repeated until about target_s seconds of CPU work have run."""
@@ -234,7 +257,7 @@ def main() -> int:
             "peak": HBM_PEAK_GBS,
             "unit": "GB/s",
             "frac": round(per_call_bytes / call_s / 1e9 / HBM_PEAK_GBS, 4),
-            "traffic": None,
+            "traffic": profiled_traffic(w.name),
             "kernel": "one ctx_decode_attn_run call (decode_split_kernel + decode_merge_kernel)",
             "bytes_per_launch": round(per_call_bytes),
             "avg_launch_us": round(call_s * 1e6, 3),
