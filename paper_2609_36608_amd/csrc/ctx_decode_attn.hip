@@ -57,7 +57,7 @@ constexpr int kXcds = 8;          // XCDs per MI355X; workgroups are dealt to th
 #ifndef CTX_ITER_BLOCKS
 #define CTX_ITER_BLOCKS 1
 #endif
-constexpr int kIterBlocks = CTX_ITER_BLOCKS;  // 16-token blocks loaded per loop trip
+[[maybe_unused]] constexpr int kIterBlocks = CTX_ITER_BLOCKS;  // 16-token blocks loaded per loop trip
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
@@ -122,6 +122,27 @@ __device__ int find_sequence(const int32_t* __restrict__ lens, int n, int64_t po
   }
   *start = carry;
   return n;
+}
+
+// Lengths of the first 64 sequences, one per lane (0 past n), with their
+// inclusive prefix sums: one load round answers totals and offsets for
+// batches of up to 64 sequences.
+struct LaneScan {
+  int64_t len;
+  int64_t incl;
+};
+
+__device__ __forceinline__ LaneScan scan_lane_lens(const int32_t* __restrict__ lens, int n, int lane) {
+  LaneScan r;
+  r.len = lane < n ? lens[lane] : 0;
+  int64_t incl = r.len;
+#pragma unroll
+  for (int off = 1; off < 64; off <<= 1) {
+    const int64_t y = __shfl_up(incl, off);
+    if (lane >= off) incl += y;
+  }
+  r.incl = incl;
+  return r;
 }
 
 __device__ __forceinline__ int64_t range_width(int64_t total, const Plan& p) {
@@ -332,10 +353,25 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(CTX_WAVES_PE
   __shared__ __attribute__((aligned(16))) uint16_t lds_v[kBlock * kHeadDim];
 #endif
 
-  const int64_t total = sum_lens(lens, p.num_seqs, lane);
-  const int64_t width = range_width(total, p);
-  const int64_t ws = (int64_t)w * width;
-  if (ws >= total) return;
+  // this wave's token range [ws, we) and the first sequence b it overlaps (span starts at pos)
+  int64_t total, width, ws, pos;
+  int b;
+  if (p.num_seqs <= 64) {
+    const LaneScan sc = scan_lane_lens(lens, p.num_seqs, lane);
+    total = __shfl(sc.incl, 63);
+    width = range_width(total, p);
+    ws = (int64_t)w * width;
+    if (ws >= total) return;
+    const unsigned long long hit = __ballot(sc.incl - sc.len <= ws && ws < sc.incl);
+    b = __ffsll(hit) - 1;
+    pos = __shfl(sc.incl - sc.len, b);
+  } else {
+    total = sum_lens(lens, p.num_seqs, lane);
+    width = range_width(total, p);
+    ws = (int64_t)w * width;
+    if (ws >= total) return;
+    b = find_sequence(lens, p.num_seqs, ws, lane, &pos);
+  }
   const int64_t we = ws + width < total ? ws + width : total;
 
   // selectors E_h: lane (c, n), slot j is 1 iff dim 8c + j == 16h + n
@@ -346,8 +382,6 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(CTX_WAVES_PE
     for (int j = 0; j < 8; ++j) sel[h][j] = (8 * c + j == 16 * h + n) ? (__bf16)1.0f : (__bf16)0.0f;
 
   const size_t row_elems = (size_t)p.hkv * kHeadDim;
-  int64_t pos;
-  int b = find_sequence(lens, p.num_seqs, ws, lane, &pos);
   while (b < p.num_seqs && pos < we) {
     const int seq_len = lens[b];
     const int64_t s0 = ws > pos ? ws - pos : 0;
@@ -466,8 +500,20 @@ __device__ __forceinline__ float lane_value(float x, int src) {
 }
 
 // One wave per (sequence, query head); lane l owns dims 2l, 2l+1.  Segment
-// weights are computed one segment per lane; the partial outputs are then
-// read eight segments at a time so their loads overlap.
+// weights are computed one segment per lane; partial outputs are read in
+// batches of kMergeBatch segments, the next batch in flight while the current
+// one is accumulated.
+constexpr int kMergeBatch = 16;
+
+__device__ __forceinline__ void load_partials(float2 (&dst)[kMergeBatch], const float* __restrict__ o_ws,
+                                              size_t first, size_t stride, int s0, int cnt, int lane) {
+#pragma unroll
+  for (int u = 0; u < kMergeBatch; ++u)
+    dst[u] = s0 + u < cnt
+                 ? reinterpret_cast<const float2*>(o_ws + (first + (size_t)(s0 + u) * stride) * kHeadDim)[lane]
+                 : make_float2(0.f, 0.f);
+}
+
 template <typename OutT>
 __global__ __launch_bounds__(64 * kMergeWaves) void decode_merge_kernel(
     const int32_t* __restrict__ lens, Plan p, const float* __restrict__ o_ws,
@@ -479,11 +525,19 @@ __global__ __launch_bounds__(64 * kMergeWaves) void decode_merge_kernel(
   const int h = gw - b * p.hq;
   const int kv = h / p.group;
   const int qi = h - kv * p.group;
-  const int seq_len = lens[b];
+  int64_t seq_len, total, pos;
+  if (p.num_seqs <= 64) {
+    const LaneScan sc = scan_lane_lens(lens, p.num_seqs, lane);
+    seq_len = __shfl(sc.len, b);
+    total = __shfl(sc.incl, 63);
+    pos = __shfl(sc.incl - sc.len, b);
+  } else {
+    seq_len = lens[b];
+    total = sum_lens(lens, p.num_seqs, lane);
+    pos = sum_lens(lens, b, lane);
+  }
   float r0 = 0.f, r1 = 0.f;
   if (seq_len > 0) {
-    const int64_t total = sum_lens(lens, p.num_seqs, lane);
-    const int64_t pos = sum_lens(lens, b, lane);
     const int64_t width = range_width(total, p);
     const int64_t wf = pos / width;
     int64_t wl = (pos + seq_len - 1) / width;
@@ -494,35 +548,38 @@ __global__ __launch_bounds__(64 * kMergeWaves) void decode_merge_kernel(
     // partial (m, l, o) of segment j lives at slot wf + j + b
     const size_t first = ((size_t)(wf + b) * p.hkv + kv) * p.group + qi;
     const size_t stride = (size_t)p.hkv * p.group;
-    float m = -INFINITY;
-    for (int j = lane; j < nseg; j += 64) m = fmaxf(m, ml_ws[first + j * stride].x);
+    float2 cur[kMergeBatch];
+    load_partials(cur, o_ws, first, stride, 0, nseg < 64 ? nseg : 64, lane);
+    const float2 ml0 = lane < nseg ? ml_ws[first + (size_t)lane * stride] : make_float2(-INFINITY, 0.f);
+    float m = ml0.x;
+    for (int j = lane + 64; j < nseg; j += 64) m = fmaxf(m, ml_ws[first + (size_t)j * stride].x);
     m = wave_max(m);
     float lsum = 0.f;
     for (int base = 0; base < nseg; base += 64) {
-      const int j = base + lane;
-      float wj = 0.f;
-      if (j < nseg) {
-        const float2 ml = ml_ws[first + j * stride];
-        wj = fast_exp2(ml.x - m);
-        lsum += wj * ml.y;
-      }
       const int cnt = nseg - base < 64 ? nseg - base : 64;
-      for (int s0 = 0; s0 < cnt; s0 += 8) {
-        float2 ov[8];
+      const float2 ml = base == 0 ? ml0
+                                  : (lane < cnt ? ml_ws[first + (size_t)(base + lane) * stride]
+                                                : make_float2(-INFINITY, 0.f));
+      const float wj = lane < cnt ? fast_exp2(ml.x - m) : 0.f;
+      lsum += wj * ml.y;
+      if (base > 0) load_partials(cur, o_ws, first + (size_t)base * stride, stride, 0, cnt, lane);
+      for (int s0 = 0; s0 < cnt; s0 += kMergeBatch) {
+        float2 nxt[kMergeBatch];
+        const bool more = s0 + kMergeBatch < cnt;
+        if (more) load_partials(nxt, o_ws, first + (size_t)base * stride, stride, s0 + kMergeBatch, cnt, lane);
 #pragma unroll
-        for (int u = 0; u < 8; ++u)
-          ov[u] = s0 + u < cnt
-                      ? reinterpret_cast<const float2*>(
-                            o_ws + (first + (size_t)(base + s0 + u) * stride) * kHeadDim)[lane]
-                      : make_float2(0.f, 0.f);
-#pragma unroll
-        for (int u = 0; u < 8; ++u) {
+        for (int u = 0; u < kMergeBatch; ++u) {
           const float wgt = lane_value(wj, (s0 + u) & 63);
-          r0 += wgt * ov[u].x;
-          r1 += wgt * ov[u].y;
+          r0 += wgt * cur[u].x;
+          r1 += wgt * cur[u].y;
+        }
+        if (more) {
+#pragma unroll
+          for (int u = 0; u < kMergeBatch; ++u) cur[u] = nxt[u];
         }
       }
     }
+#pragma unroll
     for (int off = 32; off > 0; off >>= 1) lsum += __shfl_xor(lsum, off);
     const float inv = 1.0f / lsum;
     r0 *= inv;
