@@ -32,7 +32,10 @@ HBM_BUDGET_BYTES = 240 * 2**30  # leave headroom below 288 GB for the rest of th
 
 
 def algorithmic_bytes(lens: np.ndarray, w: wl.Workload, out_bytes: int = 4) -> int:
-    """K and V rows read once (bf16), q read (bf16), out written, offsets + lengths."""
+    """K and V rows read once (bf16), q read (bf16), out written, offsets + lengths.
+    (The paged layout reads one block-table entry per page instead of an offset
+    and, when appending, reads and writes one K and V row per sequence; these
+    are left out so both layouts count the same bytes.)"""
     kv = int(lens.astype(np.int64).sum()) * w.num_kv_heads * w.head_dim * 2 * 2
     b = len(lens)
     return kv + b * w.num_q_heads * w.head_dim * (2 + out_bytes) + 8 * b
@@ -110,6 +113,8 @@ def main() -> int:
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="long_ragged", choices=sorted(wl.WORKLOADS))
     ap.add_argument("--graph", action="store_true", help="replay the timed steps from one HIP graph")
+    ap.add_argument("--paged", type=int, default=0, metavar="P",
+                    help="use P-token pages (shuffled block tables) and append each step's token")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--calibrate-copy-gib", type=float, default=0.0,
@@ -138,13 +143,21 @@ def main() -> int:
     layout = wl.workload_layout(w)
     B = w.batch
 
+    # paged layout: each sequence's capacity rounded up to whole pages
+    cache_rows = layout.num_rows
+    if args.paged:
+        if args.paged <= 0 or args.paged % 16:
+            print("bench.py: --paged takes a positive multiple of 16", file=sys.stderr)
+            return 2
+        npages = -(-layout.capacity.astype(np.int64) // args.paged)
+        cache_rows = int(npages.sum()) * args.paged
     # distinct per-layer caches; cycle fewer buffers if all layers exceed HBM
-    layer_bytes = layout.num_rows * w.num_kv_heads * w.head_dim * 2 * 2
+    layer_bytes = cache_rows * w.num_kv_heads * w.head_dim * 2 * 2
     n_buf = max(1, min(w.layers, HBM_BUDGET_BYTES // layer_bytes))
     t_setup = time.perf_counter()
     ks, vs = [], []
     for i in range(n_buf):
-        k = torch.empty((layout.num_rows, w.num_kv_heads, w.head_dim), dtype=torch.bfloat16, device=dev)
+        k = torch.empty((cache_rows, w.num_kv_heads, w.head_dim), dtype=torch.bfloat16, device=dev)
         v = torch.empty_like(k)
         wl.fill_normal_bf16_device(k, wl.DEFAULT_SEED, w.index, i, 1)
         wl.fill_normal_bf16_device(v, wl.DEFAULT_SEED, w.index, i, 2)
@@ -161,14 +174,38 @@ def main() -> int:
     torch.cuda.synchronize()
     setup_s = time.perf_counter() - t_setup
 
-    attn = DecodeAttention(w.num_q_heads, w.num_kv_heads, B, layout.max_seq_len)
+    attn = DecodeAttention(w.num_q_heads, w.num_kv_heads, B, layout.max_seq_len, page_tokens=args.paged)
     stream = torch.cuda.current_stream()
+
+    if args.paged:
+        # the same rows, viewed as pages: sequence b's capacity is cut into P-token
+        # pages whose block-table entries are shuffled over the whole cache
+        P = args.paged
+        rng = np.random.default_rng(wl.DEFAULT_SEED)
+        num_pages = cache_rows // P
+        perm = rng.permutation(num_pages).astype(np.int32)
+        bt = np.zeros((B, int(npages.max())), np.int32)
+        nxt = 0
+        for b in range(B):
+            bt[b, :npages[b]] = perm[nxt:nxt + npages[b]]
+            nxt += npages[b]
+        block_tables = torch.from_numpy(bt).to(dev)
+        pages_k = [k.view(num_pages, P, w.num_kv_heads, w.head_dim) for k in ks]
+        pages_v = [v.view(num_pages, P, w.num_kv_heads, w.head_dim) for v in vs]
+        new_k = torch.empty((B, w.num_kv_heads, w.head_dim), dtype=torch.bfloat16, device=dev)
+        new_v = torch.empty_like(new_k)
+        wl.fill_normal_bf16_device(new_k, wl.DEFAULT_SEED, w.index, 0, 3)
+        wl.fill_normal_bf16_device(new_v, wl.DEFAULT_SEED, w.index, 0, 4)
 
     def step(s: int) -> None:
         lens = lens_steps[s % w.steps]
         for layer in range(w.layers):
-            attn.run(qs[layer], ks[layer % n_buf], vs[layer % n_buf], offsets, lens, w.scale,
-                     outs[layer], stream=stream)
+            if args.paged:
+                attn.run_paged(qs[layer], pages_k[layer % n_buf], pages_v[layer % n_buf], block_tables, lens,
+                               w.scale, outs[layer], k_new=new_k, v_new=new_v, stream=stream)
+            else:
+                attn.run(qs[layer], ks[layer % n_buf], vs[layer % n_buf], offsets, lens, w.scale,
+                         outs[layer], stream=stream)
 
     for i in range(args.warmup):
         step(i)
@@ -246,6 +283,7 @@ def main() -> int:
             "distinct_layer_buffers": n_buf,
             "seed": wl.DEFAULT_SEED,
             "launch": "hip_graph" if graph is not None else "stream",
+            "kv_layout": f"paged, {args.paged}-token pages, appends each step's token" if args.paged else "contiguous",
             "parallelism": "none (1 GPU)",
         },
         "frac_of_hbm_peak": round(gbs / HBM_PEAK_GBS, 4),

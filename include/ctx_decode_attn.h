@@ -67,7 +67,10 @@ typedef struct {
   ctx_dtype out_dtype;  /* F32, or BF16 = round-to-nearest-even of the fp32 result */
   int32_t split_tokens; /* 0: balanced split of the batch's tokens over the GPU (default);
                            >= 16: every work range holds exactly this many tokens
-                           (tests use it to force split boundaries) */
+                           (tests use it to force split boundaries; a multiple of 16
+                           when page_tokens > 0) */
+  int32_t page_tokens;  /* tokens per cache page for ctx_decode_attn_run_paged: 0 (contiguous
+                           caches only) or a positive multiple of 16 */
 } ctx_decode_attn_desc;
 
 /*
@@ -111,6 +114,36 @@ int ctx_decode_attn_create(const ctx_decode_attn_desc* desc, ctx_decode_attn** o
 int ctx_decode_attn_run(ctx_decode_attn* handle, const void* q, const void* k_cache,
                         const void* v_cache, const int32_t* seq_offsets, const int32_t* seq_lens,
                         int32_t num_seqs, float scale, void* out, void* stream);
+
+/*
+ * Paged variant of ctx_decode_attn_run: the caches are split into pages of
+ * P = desc.page_tokens tokens, as in the block tables of the paged-attention
+ * serving engine the paper rolls out with (Sec. 5.1, vLLM; prefix caching is
+ * off, tab:training-hyperparameters), and the step can append the token it
+ * decodes (the token context grows by one token per step, eq:token-context).
+ *
+ *   q            bf16 [num_seqs, Hq, D]
+ *   k_pages      bf16 [num_pages, P, Hkv, D]: token t of sequence b is slot t % P of
+ *   v_pages      page block_tables[b][t / P] (same layout for V)
+ *   block_tables int32 [num_seqs, max_pages_per_seq], row-major; entries
+ *                0 .. ceil(seq_lens[b] / P) - 1 of row b must name valid pages
+ *   seq_lens     int32 [num_seqs]: tokens attended, the new one included
+ *   k_new, v_new bf16 [num_seqs, Hkv, D] or both NULL.  If given, the key and value
+ *                of token seq_lens[b] - 1 are taken from them and also written
+ *                into that token's cache slot (what the slot held before is never
+ *                used); sequences with seq_lens[b] = 0 append nothing
+ *   out          [num_seqs, Hq, D] of desc.out_dtype
+ *
+ * A page holding tokens of a sequence that appends must not be shared with
+ * another sequence in the same call.  Same asynchrony, determinism and
+ * ownership rules as ctx_decode_attn_run.
+ * Errors: INVALID_ARG, CAPACITY, ALIGNMENT, HIP; UNSUPPORTED if the handle was
+ * created with page_tokens = 0.
+ */
+int ctx_decode_attn_run_paged(ctx_decode_attn* handle, const void* q, void* k_pages, void* v_pages,
+                              const int32_t* block_tables, int32_t max_pages_per_seq,
+                              const int32_t* seq_lens, int32_t num_seqs, const void* k_new,
+                              const void* v_new, float scale, void* out, void* stream);
 
 /* Wait for the handle's device, free the workspace and the handle.  NULL is a no-op. */
 int ctx_decode_attn_destroy(ctx_decode_attn* handle);

@@ -30,6 +30,9 @@ def _load():
         lib.oracle_decode_attn_pairs.restype = ctypes.c_int
         lib.oracle_attn_weights.argtypes = [p, p, p, p, i32, i32, i32, i32, i64, f64, i32, i32, p]
         lib.oracle_attn_weights.restype = ctypes.c_int
+        lib.oracle_decode_attn_paged_pairs.argtypes = [p, p, p, p, i32, i32, i64, p, i32, i32, i32, i32,
+                                                       f64, p, p, p, i64, p, i32]
+        lib.oracle_decode_attn_paged_pairs.restype = ctypes.c_int
         _lib = lib
     return _lib
 
@@ -92,3 +95,33 @@ def attn_weights(q, k, seq_offsets, seq_lens, scale, b: int, h: int) -> np.ndarr
     _check(_load().oracle_attn_weights(_ptr(q), _ptr(k), _ptr(offs), _ptr(lens), nb, hq, hkv, d,
                                        rows, float(scale), b, h, _ptr(w)))
     return w[: int(lens[b])]
+
+
+def decode_attn_paged(q, k_pages, v_pages, block_tables, seq_lens, scale, k_new=None, v_new=None,
+                      pairs=None, threads: int = 0) -> np.ndarray:
+    """Paged decode attention: k_pages, v_pages [num_pages, P, Hkv, D] bf16 bits,
+    block_tables [B, max_pages] int32; optional k_new, v_new [B, Hkv, D] replace
+    each sequence's newest token.  Returns [B, Hq, D] (or [n_pairs, D])."""
+    q, k, v = _u16(q), _u16(k_pages), _u16(v_pages)
+    bt, lens = _i32(block_tables), _i32(seq_lens)
+    b, hq, d = q.shape
+    num_pages, page_tokens, hkv, dk = k.shape
+    if v.shape != k.shape or dk != d or bt.ndim != 2 or bt.shape[0] != b or len(lens) != b:
+        raise ValueError("shape mismatch")
+    if (k_new is None) != (v_new is None):
+        raise ValueError("k_new and v_new go together")
+    kn = _u16(k_new) if k_new is not None else None
+    vn = _u16(v_new) if v_new is not None else None
+    if pairs is None:
+        pairs = np.stack(np.meshgrid(np.arange(b), np.arange(hq), indexing="ij"), -1).reshape(-1, 2)
+        shape = (b, hq, d)
+    else:
+        shape = None
+    pairs = np.ascontiguousarray(pairs, dtype=np.int32).reshape(-1, 2)
+    out = np.zeros((len(pairs), d), dtype=np.float64)
+    nullp = ctypes.c_void_p(0)
+    _check(_load().oracle_decode_attn_paged_pairs(
+        _ptr(q), _ptr(k), _ptr(v), _ptr(bt), bt.shape[1], page_tokens, num_pages, _ptr(lens), b, hq, hkv,
+        d, float(scale), _ptr(kn) if kn is not None else nullp, _ptr(vn) if vn is not None else nullp,
+        _ptr(pairs), len(pairs), _ptr(out), threads))
+    return out.reshape(shape) if shape is not None else out

@@ -31,6 +31,13 @@
  *   q    uint16 bf16 bits [B, Hq, D]
  *   K, V uint16 bf16 bits [num_rows, Hkv, D]
  *   out  double [B, Hq, D]
+ *
+ * Paged caches (the serving engine's block tables, Sec. 5.1 / App. training
+ * setup: vLLM with prefix caching disabled): token t of sequence b lives in
+ * cache row  block_tables[b][t / P] * P + t % P  of [num_pages * P, Hkv, D].
+ * With k_new / v_new given, the sequence's newest token (t = L_b - 1) takes
+ * its key and value from those arrays instead of the cache: the decode step
+ * appends the token it is decoding (eq:token-context grows by one token).
  * Parity: pinned (closed forms, brute force, invariants; see the tests).
  */
 #include <math.h>
@@ -224,4 +231,136 @@ int oracle_attn_weights(const uint16_t *q, const uint16_t *k,
     if (b < 0 || b >= num_seqs || h < 0 || h >= hq)
         return ORACLE_ERR_ARG;
     return weights_one(q, k, seq_offsets, seq_lens, b, h, hq, hkv, d, num_rows, scale, w);
+}
+
+/* ---------------------------------------------------------------- paged */
+
+typedef struct {
+    const int32_t *block_tables; /* [num_seqs, max_pages] */
+    int32_t max_pages;
+    int32_t page_tokens;
+    int64_t num_pages;
+    const uint16_t *k_new; /* [num_seqs, Hkv, D] or NULL */
+    const uint16_t *v_new;
+} paged_view;
+
+/* Cache row of token t of sequence b, or -1 if the block table points outside the cache. */
+static int64_t paged_row(const paged_view *pv, int32_t b, int64_t t)
+{
+    if (t / pv->page_tokens >= pv->max_pages)
+        return -1;
+    const int64_t page = pv->block_tables[(int64_t)b * pv->max_pages + t / pv->page_tokens];
+    if (page < 0 || page >= pv->num_pages)
+        return -1;
+    return page * pv->page_tokens + t % pv->page_tokens;
+}
+
+/* Key (or value) row of token t of sequence b for KV head kv, after the append. */
+static const uint16_t *paged_vec(const paged_view *pv, const uint16_t *cache, const uint16_t *fresh,
+                                 int32_t b, int64_t t, int64_t len, int32_t kv, int32_t hkv, int32_t d)
+{
+    if (fresh != NULL && t == len - 1)
+        return fresh + ((int64_t)b * hkv + kv) * d;
+    const int64_t r = paged_row(pv, b, t);
+    return r < 0 ? NULL : cache + (r * hkv + kv) * d;
+}
+
+/* Same definition as attend_one, reading rows through the block table. */
+static int attend_one_paged(const uint16_t *q, const uint16_t *k, const uint16_t *v,
+                            const paged_view *pv, const int32_t *seq_lens, int32_t b, int32_t h,
+                            int32_t hq, int32_t hkv, int32_t d, double scale, double *w, double *out)
+{
+    const int32_t kv = h / (hq / hkv);
+    const int64_t len = seq_lens[b];
+    for (int32_t i = 0; i < d; ++i)
+        out[i] = 0.0;
+    if (len < 0)
+        return ORACLE_ERR_RANGE;
+    if (len == 0)
+        return ORACLE_OK;
+    const uint16_t *qrow = q + ((int64_t)b * hq + h) * d;
+    double smax = -INFINITY;
+    for (int64_t t = 0; t < len; ++t) {
+        const uint16_t *krow = paged_vec(pv, k, pv->k_new, b, t, len, kv, hkv, d);
+        if (krow == NULL)
+            return ORACLE_ERR_RANGE;
+        double dot = 0.0;
+        for (int32_t i = 0; i < d; ++i)
+            dot += bf16_value(qrow[i]) * bf16_value(krow[i]);
+        w[t] = scale * dot;
+        if (w[t] > smax)
+            smax = w[t];
+    }
+    double z = 0.0;
+    for (int64_t t = 0; t < len; ++t) {
+        w[t] = exp(w[t] - smax);
+        z += w[t];
+    }
+    for (int64_t t = 0; t < len; ++t) {
+        const uint16_t *vrow = paged_vec(pv, v, pv->v_new, b, t, len, kv, hkv, d);
+        if (vrow == NULL)
+            return ORACLE_ERR_RANGE;
+        for (int32_t i = 0; i < d; ++i)
+            out[i] += (w[t] / z) * bf16_value(vrow[i]);
+    }
+    return ORACLE_OK;
+}
+
+/*
+ * Paged decode attention for selected (sequence, query head) pairs (pairs as
+ * in oracle_decode_attn_pairs).  k_pages, v_pages: [num_pages * page_tokens,
+ * Hkv, D]; block_tables: [num_seqs, max_pages]; k_new, v_new: [num_seqs, Hkv,
+ * D] or NULL (no append).
+ */
+int oracle_decode_attn_paged_pairs(const uint16_t *q, const uint16_t *k_pages, const uint16_t *v_pages,
+                                   const int32_t *block_tables, int32_t max_pages, int32_t page_tokens,
+                                   int64_t num_pages, const int32_t *seq_lens, int32_t num_seqs,
+                                   int32_t hq, int32_t hkv, int32_t d, double scale,
+                                   const uint16_t *k_new, const uint16_t *v_new,
+                                   const int32_t *pairs, int64_t num_pairs, double *out,
+                                   int32_t num_threads)
+{
+    int rc = check_shape(num_seqs, hq, hkv, d);
+    if (rc != ORACLE_OK)
+        return rc;
+    if (page_tokens <= 0 || max_pages < 0 || num_pages < 0 || (k_new == NULL) != (v_new == NULL))
+        return ORACLE_ERR_ARG;
+    for (int64_t i = 0; i < num_pairs; ++i)
+        if (pairs[2 * i] < 0 || pairs[2 * i] >= num_seqs || pairs[2 * i + 1] < 0 ||
+            pairs[2 * i + 1] >= hq)
+            return ORACLE_ERR_ARG;
+    const paged_view pv = {block_tables, max_pages, page_tokens, num_pages, k_new, v_new};
+    const int64_t lmax = max_len(seq_lens, num_seqs);
+    int status = ORACLE_OK;
+#ifdef _OPENMP
+    if (num_threads <= 0)
+        num_threads = omp_get_max_threads();
+#pragma omp parallel num_threads(num_threads)
+#endif
+    {
+        double *w = (double *)malloc((size_t)(lmax > 0 ? lmax : 1) * sizeof(double));
+        if (w == NULL) {
+#ifdef _OPENMP
+#pragma omp atomic write
+#endif
+            status = ORACLE_ERR_NOMEM;
+        }
+#ifdef _OPENMP
+#pragma omp for schedule(dynamic, 1)
+#endif
+        for (int64_t i = 0; i < num_pairs; ++i) {
+            if (w == NULL)
+                continue;
+            int r = attend_one_paged(q, k_pages, v_pages, &pv, seq_lens, pairs[2 * i],
+                                     pairs[2 * i + 1], hq, hkv, d, scale, w, out + i * d);
+            if (r != ORACLE_OK) {
+#ifdef _OPENMP
+#pragma omp atomic write
+#endif
+                status = r;
+            }
+        }
+        free(w);
+    }
+    return status;
 }

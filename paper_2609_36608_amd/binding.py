@@ -26,6 +26,7 @@ CTX_DTYPE_F32 = 1
 EXPORTS = (
     "ctx_decode_attn_create",
     "ctx_decode_attn_run",
+    "ctx_decode_attn_run_paged",
     "ctx_decode_attn_destroy",
     "ctx_decode_attn_status_string",
     "ctx_decode_attn_last_error",
@@ -41,6 +42,7 @@ class CtxDesc(ctypes.Structure):
         ("max_seq_len", ctypes.c_int32),
         ("out_dtype", ctypes.c_int),
         ("split_tokens", ctypes.c_int32),
+        ("page_tokens", ctypes.c_int32),
     ]
 
 
@@ -71,6 +73,8 @@ def load_library(path: str | None = None):
     lib.ctx_decode_attn_create.restype = ctypes.c_int
     lib.ctx_decode_attn_run.argtypes = [vp, vp, vp, vp, vp, vp, i32, ctypes.c_float, vp, vp]
     lib.ctx_decode_attn_run.restype = ctypes.c_int
+    lib.ctx_decode_attn_run_paged.argtypes = [vp, vp, vp, vp, vp, i32, vp, i32, vp, vp, ctypes.c_float, vp, vp]
+    lib.ctx_decode_attn_run_paged.restype = ctypes.c_int
     lib.ctx_decode_attn_destroy.argtypes = [vp]
     lib.ctx_decode_attn_destroy.restype = ctypes.c_int
     lib.ctx_decode_attn_status_string.argtypes = [ctypes.c_int]
@@ -103,13 +107,13 @@ class DecodeAttention:
     per sequence over ragged KV caches [rows, Hkv, 128] (bf16)."""
 
     def __init__(self, num_q_heads: int, num_kv_heads: int, max_batch: int, max_seq_len: int,
-                 head_dim: int = 128, out_dtype=None, split_tokens: int = 0):
+                 head_dim: int = 128, out_dtype=None, split_tokens: int = 0, page_tokens: int = 0):
         import torch
 
         self.lib = load_library()
         self.out_dtype = torch.float32 if out_dtype is None else out_dtype
         self.desc = CtxDesc(num_q_heads, num_kv_heads, head_dim, max_batch, max_seq_len,
-                            _dtype_code(self.out_dtype), split_tokens)
+                            _dtype_code(self.out_dtype), split_tokens, page_tokens)
         handle = ctypes.c_void_p()
         rc = self.lib.ctx_decode_attn_create(ctypes.byref(self.desc), ctypes.byref(handle))
         if rc != CTX_OK:
@@ -145,6 +149,52 @@ class DecodeAttention:
         rc = self.lib.ctx_decode_attn_run(self.handle, q.data_ptr(), k_cache.data_ptr(), v_cache.data_ptr(),
                                           seq_offsets.data_ptr(), seq_lens.data_ptr(), b, float(scale),
                                           out.data_ptr(), sp)
+        if rc != CTX_OK:
+            raise error_for(self.lib, rc)
+        return out
+
+    def run_paged(self, q, k_pages, v_pages, block_tables, seq_lens, scale: float, out,
+                  k_new=None, v_new=None, stream=None):
+        """Paged caches [num_pages, P, Hkv, D]; block_tables [B, max_pages] int32;
+        optional k_new / v_new [B, Hkv, D] are appended as each sequence's
+        newest token (written into its cache slot)."""
+        import torch
+
+        if self.handle is None:
+            raise RuntimeError("handle is closed")
+        d = self.desc
+        if (k_new is None) != (v_new is None):
+            raise ValueError("k_new and v_new go together")
+        checks = [("q", q, torch.bfloat16), ("k_pages", k_pages, torch.bfloat16),
+                  ("v_pages", v_pages, torch.bfloat16), ("block_tables", block_tables, torch.int32),
+                  ("seq_lens", seq_lens, torch.int32), ("out", out, self.out_dtype)]
+        if k_new is not None:
+            checks += [("k_new", k_new, torch.bfloat16), ("v_new", v_new, torch.bfloat16)]
+        for name, t, dt in checks:
+            if t.dtype != dt:
+                raise TypeError(f"{name} must be {dt}, got {t.dtype}")
+            if not t.is_cuda or t.device.index != self.device:
+                raise ValueError(f"{name} must be on cuda:{self.device}")
+            if not t.is_contiguous():
+                raise ValueError(f"{name} must be contiguous")
+        b = q.shape[0]
+        if q.shape != (b, d.num_q_heads, d.head_dim) or out.shape != q.shape:
+            raise ValueError(f"q/out must be [{b}, {d.num_q_heads}, {d.head_dim}]")
+        if k_pages.dim() != 4 or k_pages.shape[1:] != (d.page_tokens, d.num_kv_heads, d.head_dim) \
+                or v_pages.shape != k_pages.shape:
+            raise ValueError(f"k_pages/v_pages must be [pages, {d.page_tokens}, {d.num_kv_heads}, {d.head_dim}]")
+        if block_tables.dim() != 2 or block_tables.shape[0] != b or seq_lens.shape != (b,):
+            raise ValueError(f"block_tables must be [{b}, max_pages] and seq_lens [{b}]")
+        if k_new is not None and (k_new.shape != (b, d.num_kv_heads, d.head_dim) or v_new.shape != k_new.shape):
+            raise ValueError(f"k_new/v_new must be [{b}, {d.num_kv_heads}, {d.head_dim}]")
+        if stream is None:
+            stream = torch.cuda.current_stream()
+        sp = stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream)
+        rc = self.lib.ctx_decode_attn_run_paged(
+            self.handle, q.data_ptr(), k_pages.data_ptr(), v_pages.data_ptr(), block_tables.data_ptr(),
+            block_tables.shape[1], seq_lens.data_ptr(), b,
+            k_new.data_ptr() if k_new is not None else None, v_new.data_ptr() if v_new is not None else None,
+            float(scale), out.data_ptr(), sp)
         if rc != CTX_OK:
             raise error_for(self.lib, rc)
         return out

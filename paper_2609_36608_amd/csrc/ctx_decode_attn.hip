@@ -54,10 +54,6 @@ constexpr int kXcds = 8;          // XCDs per MI355X; workgroups are dealt to th
 #ifndef CTX_WAVES_PER_EU
 #define CTX_WAVES_PER_EU 3
 #endif
-#ifndef CTX_ITER_BLOCKS
-#define CTX_ITER_BLOCKS 1
-#endif
-[[maybe_unused]] constexpr int kIterBlocks = CTX_ITER_BLOCKS;  // 16-token blocks loaded per loop trip
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
@@ -73,7 +69,19 @@ struct Plan {
   int32_t group;
   int32_t num_ranges;    // ranges in the grid (each = hkv workgroups)
   int32_t forced_width;  // > 0: fixed tokens per range
+  int32_t pad;           // sequences occupy round_up(L, pad) tokens of the flattened batch
   float scale_log2;      // scale * log2(e)
+};
+
+// Paged layout: token t of sequence b is row block_tables[b][t / P] * P + t % P.
+struct Paged {
+  const int32_t* block_tables;  // [num_seqs, max_pages]
+  int32_t max_pages;
+  int32_t page_tokens;          // P, a multiple of kBlock
+  const uint16_t* k_new;        // [num_seqs, Hkv, D] appended token, or null
+  const uint16_t* v_new;
+  uint16_t* k_cache;            // the caches, for writing the appended row
+  uint16_t* v_cache;
 };
 
 // ------------------------------------------------------------ wave helpers
@@ -90,21 +98,24 @@ __device__ __forceinline__ float wave_max(float x) {
   return x;
 }
 
-// sum of lens[0 .. n)
-__device__ __forceinline__ int64_t sum_lens(const int32_t* __restrict__ lens, int n, int lane) {
+// Tokens a sequence of length len occupies in the flattened batch.
+__device__ __forceinline__ int64_t padded(int64_t len, int pad) { return (len + pad - 1) / pad * pad; }
+
+// sum of the padded lens[0 .. n)
+__device__ __forceinline__ int64_t sum_lens(const int32_t* __restrict__ lens, int n, int lane, int pad) {
   int64_t acc = 0;
-  for (int i = lane; i < n; i += 64) acc += lens[i];
+  for (int i = lane; i < n; i += 64) acc += padded(lens[i], pad);
   return wave_sum(acc);
 }
 
 // First sequence b whose flattened span [P_b, P_b + L_b) contains pos; *start = P_b.
 // Returns n if none.
 __device__ int find_sequence(const int32_t* __restrict__ lens, int n, int64_t pos, int lane,
-                             int64_t* start) {
+                             int64_t* start, int pad) {
   int64_t carry = 0;
   for (int base = 0; base < n; base += 64) {
     const int i = base + lane;
-    const int64_t len = i < n ? lens[i] : 0;
+    const int64_t len = i < n ? padded(lens[i], pad) : 0;
     int64_t incl = len;
 #pragma unroll
     for (int off = 1; off < 64; off <<= 1) {
@@ -124,7 +135,7 @@ __device__ int find_sequence(const int32_t* __restrict__ lens, int n, int64_t po
   return n;
 }
 
-// Lengths of the first 64 sequences, one per lane (0 past n), with their
+// Padded lengths of the first 64 sequences, one per lane (0 past n), with their
 // inclusive prefix sums: one load round answers totals and offsets for
 // batches of up to 64 sequences.
 struct LaneScan {
@@ -132,9 +143,10 @@ struct LaneScan {
   int64_t incl;
 };
 
-__device__ __forceinline__ LaneScan scan_lane_lens(const int32_t* __restrict__ lens, int n, int lane) {
+__device__ __forceinline__ LaneScan scan_lane_lens(const int32_t* __restrict__ lens, int n, int lane,
+                                                   int pad) {
   LaneScan r;
-  r.len = lane < n ? lens[lane] : 0;
+  r.len = lane < n ? padded(lens[lane], pad) : 0;
   int64_t incl = r.len;
 #pragma unroll
   for (int off = 1; off < 64; off <<= 1) {
@@ -168,14 +180,8 @@ __device__ __forceinline__ s16x4 pack_bf16x4(float a, float b, float c, float d)
 
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 
-#ifndef CTX_LDS_STAGE
-#define CTX_LDS_STAGE 1
-#endif
 #ifndef CTX_NT_LOADS
-#define CTX_NT_LOADS CTX_LDS_STAGE
-#endif
-#ifndef CTX_PREFETCH
-#define CTX_PREFETCH 0
+#define CTX_NT_LOADS 1
 #endif
 
 __device__ __forceinline__ u32x4 load16(const uint16_t* p) {
@@ -202,38 +208,6 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const uint16_t* base
 
 __device__ __forceinline__ u32x4 buf_load16(__amdgpu_buffer_rsrc_t r, int voff, int soff) {
   return __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, kLoadAux));
-}
-
-// One lane's share of a 16-token block of one KV head: token `tok` (relative
-// to the segment), the 4 x 16-byte pieces at dims 32*kk + 8*c .. +8.
-// `base` already points at dim 8*c of the segment's first row for this head.
-template <bool kPred>
-__device__ __forceinline__ void load_block(u32x4 (&r)[4], const uint16_t* __restrict__ base,
-                                           size_t row_elems, int tok, int len) {
-  if (!kPred || tok < len) {
-    const uint16_t* ptr = base + (size_t)tok * row_elems;
-#pragma unroll
-    for (int kk = 0; kk < 4; ++kk) r[kk] = load16(ptr + 32 * kk);
-  } else {
-#pragma unroll
-    for (int kk = 0; kk < 4; ++kk) r[kk] = u32x4{0u, 0u, 0u, 0u};
-  }
-}
-
-// Coalesced share of a 16-token block: lane l loads 16 bytes (chunk l % 16) of
-// tokens tok, tok + 4, tok + 8, tok + 12 (tok = l / 16 + block start).
-// `base` already points at the lane's chunk of the segment's first row.
-template <bool kPred>
-__device__ __forceinline__ void load_coalesced(u32x4 (&r)[4], const uint16_t* __restrict__ base,
-                                               size_t row_elems, int tok, int len) {
-#pragma unroll
-  for (int u = 0; u < 4; ++u) {
-    const int t = tok + 4 * u;
-    if (!kPred || t < len)
-      r[u] = load16(base + (size_t)t * row_elems);
-    else
-      r[u] = u32x4{0u, 0u, 0u, 0u};
-  }
 }
 
 // Softmax state of one lane: query head n of the group (lanes with n >= g
@@ -331,11 +305,11 @@ __device__ __forceinline__ void store2<uint16_t>(uint16_t* dst, float a, float b
 
 // ------------------------------------------------------------ split kernel
 
-template <typename OutT>
+template <typename OutT, bool kPaged>
 __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(CTX_WAVES_PER_EU))) void decode_split_kernel(
     const uint16_t* __restrict__ q, const uint16_t* __restrict__ kc,
     const uint16_t* __restrict__ vc, const int32_t* __restrict__ offs,
-    const int32_t* __restrict__ lens, Plan p, float* __restrict__ o_ws,
+    const int32_t* __restrict__ lens, Plan p, Paged pg, float* __restrict__ o_ws,
     float2* __restrict__ ml_ws, OutT* __restrict__ out) {
   const int lane = threadIdx.x;
   const int n = lane & 15;
@@ -348,16 +322,14 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(CTX_WAVES_PE
   const int kv = blockIdx.x / p.num_ranges;
   const int w = blockIdx.x - kv * p.num_ranges;
   const int g = p.group;
-#if CTX_LDS_STAGE
   __shared__ __attribute__((aligned(16))) uint16_t lds_k[kBlock * kHeadDim];
   __shared__ __attribute__((aligned(16))) uint16_t lds_v[kBlock * kHeadDim];
-#endif
 
   // this wave's token range [ws, we) and the first sequence b it overlaps (span starts at pos)
   int64_t total, width, ws, pos;
   int b;
   if (p.num_seqs <= 64) {
-    const LaneScan sc = scan_lane_lens(lens, p.num_seqs, lane);
+    const LaneScan sc = scan_lane_lens(lens, p.num_seqs, lane, p.pad);
     total = __shfl(sc.incl, 63);
     width = range_width(total, p);
     ws = (int64_t)w * width;
@@ -366,11 +338,11 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(CTX_WAVES_PE
     b = __ffsll(hit) - 1;
     pos = __shfl(sc.incl - sc.len, b);
   } else {
-    total = sum_lens(lens, p.num_seqs, lane);
+    total = sum_lens(lens, p.num_seqs, lane, p.pad);
     width = range_width(total, p);
     ws = (int64_t)w * width;
     if (ws >= total) return;
-    b = find_sequence(lens, p.num_seqs, ws, lane, &pos);
+    b = find_sequence(lens, p.num_seqs, ws, lane, &pos, p.pad);
   }
   const int64_t we = ws + width < total ? ws + width : total;
 
@@ -402,11 +374,27 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(CTX_WAVES_PE
 #pragma unroll
       for (int nb = 0; nb < 8; ++nb) o[nb] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-      const uint16_t* kseg = kc + ((size_t)offs[b] + (size_t)s0) * row_elems + (size_t)kv * kHeadDim;
-      const uint16_t* vseg = vc + ((size_t)offs[b] + (size_t)s0) * row_elems + (size_t)kv * kHeadDim;
       const int row_bytes = (int)(row_elems * 2);
-      const size_t blk_elems = (size_t)kBlock * row_elems;
-#if CTX_LDS_STAGE
+      // Contiguous layout: the segment's rows follow each other from row
+      // offs[b] + s0.  Paged layout: s0 is a multiple of kBlock (lengths are
+      // padded to kBlock in the range plan), so every block lies inside one
+      // page; the page numbers of up to 64 pages of the segment are held one
+      // per lane and refreshed when the segment runs past them.
+      const uint16_t* kseg = kc + (size_t)kv * kHeadDim;
+      const uint16_t* vseg = vc + (size_t)kv * kHeadDim;
+      int page_lane = 0, page_base = 0;
+      if (kPaged) {
+        page_base = (int)(s0 / pg.page_tokens);
+        const int used = (int)((seq_len + pg.page_tokens - 1) / pg.page_tokens);
+        const int j = page_base + lane;
+        page_lane = j < used && j < pg.max_pages ? pg.block_tables[(size_t)b * pg.max_pages + j] : 0;
+      } else {
+        kseg += ((size_t)offs[b] + (size_t)s0) * row_elems;
+        vseg += ((size_t)offs[b] + (size_t)s0) * row_elems;
+      }
+      // the appended token (paged, with k_new): the last token of a sequence
+      const bool append = kPaged && pg.k_new != nullptr && s1 == seq_len;
+
       // Coalesced loads: 16 lanes cover one token's 256-byte head slice, four
       // tokens per instruction.  The block goes through a wave-private LDS
       // tile (16-byte chunks XOR-swizzled by token, conflict-free both ways)
@@ -414,9 +402,26 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(CTX_WAVES_PE
       const int voff = (lane >> 4) * row_bytes + (lane & 15) * 16;
       const int ld_tok = lane >> 4;
       for (int t = 0; t < len; t += kBlock) {
-        const uint32_t bytes = (uint32_t)((len - t < kBlock ? len - t : kBlock) * row_bytes);
-        const __amdgpu_buffer_rsrc_t rk = make_rsrc(kseg + (size_t)(t / kBlock) * blk_elems, bytes);
-        const __amdgpu_buffer_rsrc_t rv = make_rsrc(vseg + (size_t)(t / kBlock) * blk_elems, bytes);
+        const int valid = len - t < kBlock ? len - t : kBlock;
+        size_t blk_row;  // first cache row of the block
+        if (kPaged) {
+          const int64_t tok = s0 + t;
+          int pj = (int)(tok / pg.page_tokens) - page_base;
+          if (pj >= 64) {  // the segment ran past the pages held in registers
+            page_base += 64;
+            pj -= 64;
+            const int used = (int)((seq_len + pg.page_tokens - 1) / pg.page_tokens);
+            const int j = page_base + lane;
+            page_lane = j < used && j < pg.max_pages ? pg.block_tables[(size_t)b * pg.max_pages + j] : 0;
+          }
+          const int page = __builtin_amdgcn_readlane(page_lane, pj);
+          blk_row = (size_t)page * pg.page_tokens + (size_t)(tok % pg.page_tokens);
+        } else {
+          blk_row = (size_t)t;
+        }
+        const uint32_t bytes = (uint32_t)(valid * row_bytes);
+        const __amdgpu_buffer_rsrc_t rk = make_rsrc(kseg + blk_row * row_elems, bytes);
+        const __amdgpu_buffer_rsrc_t rv = make_rsrc(vseg + blk_row * row_elems, bytes);
         u32x4 pk[4], pv[4];
 #pragma unroll
         for (int u = 0; u < 4; ++u) {
@@ -431,6 +436,22 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(CTX_WAVES_PE
           *reinterpret_cast<u32x4*>(&lds_k[slot]) = pk[u];
           *reinterpret_cast<u32x4*>(&lds_v[slot]) = pv[u];
         }
+        if (append && t + kBlock >= len) {
+          // the block holding the newest token: attend to the appended row and
+          // write it into the cache (16 lanes, 16 bytes each)
+          const int tok = valid - 1;
+          if (lane < 16) {
+            const size_t src = ((size_t)b * p.hkv + kv) * kHeadDim + 8 * lane;
+            const u32x4 nk = load16(pg.k_new + src);
+            const u32x4 nv = load16(pg.v_new + src);
+            const int slot = tok * kHeadDim + ((lane ^ tok) << 3);
+            *reinterpret_cast<u32x4*>(&lds_k[slot]) = nk;
+            *reinterpret_cast<u32x4*>(&lds_v[slot]) = nv;
+            const size_t dst = (blk_row + tok) * row_elems + (size_t)kv * kHeadDim + 8 * lane;
+            *reinterpret_cast<u32x4*>(pg.k_cache + dst) = nk;
+            *reinterpret_cast<u32x4*>(pg.v_cache + dst) = nv;
+          }
+        }
         __syncthreads();
         u32x4 kr[4], vr[4];
 #pragma unroll
@@ -439,34 +460,8 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(CTX_WAVES_PE
           kr[kk] = *reinterpret_cast<const u32x4*>(&lds_k[slot]);
           vr[kk] = *reinterpret_cast<const u32x4*>(&lds_v[slot]);
         }
-        attend_block(kr, vr, qb, sel, len - t < kBlock ? len - t : kBlock, c, p.scale_log2, st, o);
+        attend_block(kr, vr, qb, sel, valid, c, p.scale_log2, st, o);
       }
-#else
-      // Loads straight into the MFMA operand layout: lane (c, n) reads token n,
-      // bytes 64*kk + 16*c of the head slice.
-      const int voff = n * row_bytes + c * 16;
-      for (int t = 0; t < len; t += kIterBlocks * kBlock) {
-        u32x4 kr[kIterBlocks][4], vr[kIterBlocks][4];
-#pragma unroll
-        for (int i = 0; i < kIterBlocks; ++i) {
-          const int tb = t + i * kBlock;
-          const int rem = len - tb;
-          const uint32_t bytes = (uint32_t)((rem <= 0 ? 0 : rem < kBlock ? rem : kBlock) * row_bytes);
-          const __amdgpu_buffer_rsrc_t rk = make_rsrc(kseg + (size_t)(tb / kBlock) * blk_elems, bytes);
-          const __amdgpu_buffer_rsrc_t rv = make_rsrc(vseg + (size_t)(tb / kBlock) * blk_elems, bytes);
-#pragma unroll
-          for (int kk = 0; kk < 4; ++kk) {
-            kr[i][kk] = buf_load16(rk, voff + 64 * kk, 0);
-            vr[i][kk] = buf_load16(rv, voff + 64 * kk, 0);
-          }
-        }
-#pragma unroll
-        for (int i = 0; i < kIterBlocks; ++i) {
-          const int rem = len - (t + i * kBlock);
-          if (rem > 0) attend_block(kr[i], vr[i], qb, sel, rem < kBlock ? rem : kBlock, c, p.scale_log2, st, o);
-        }
-      }
-#endif
 
       float l_tot = st.l + __shfl_xor(st.l, 16);
       l_tot += __shfl_xor(l_tot, 32);
@@ -488,7 +483,7 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(CTX_WAVES_PE
         }
       }
     }
-    pos += seq_len;
+    pos += padded(seq_len, p.pad);
     ++b;
   }
 }
@@ -503,7 +498,10 @@ __device__ __forceinline__ float lane_value(float x, int src) {
 // weights are computed one segment per lane; partial outputs are read in
 // batches of kMergeBatch segments, the next batch in flight while the current
 // one is accumulated.
-constexpr int kMergeBatch = 16;
+#ifndef CTX_MERGE_BATCH
+#define CTX_MERGE_BATCH 16
+#endif
+constexpr int kMergeBatch = CTX_MERGE_BATCH;
 
 __device__ __forceinline__ void load_partials(float2 (&dst)[kMergeBatch], const float* __restrict__ o_ws,
                                               size_t first, size_t stride, int s0, int cnt, int lane) {
@@ -526,15 +524,14 @@ __global__ __launch_bounds__(64 * kMergeWaves) void decode_merge_kernel(
   const int kv = h / p.group;
   const int qi = h - kv * p.group;
   int64_t seq_len, total, pos;
+  seq_len = lens[b];
   if (p.num_seqs <= 64) {
-    const LaneScan sc = scan_lane_lens(lens, p.num_seqs, lane);
-    seq_len = __shfl(sc.len, b);
+    const LaneScan sc = scan_lane_lens(lens, p.num_seqs, lane, p.pad);
     total = __shfl(sc.incl, 63);
     pos = __shfl(sc.incl - sc.len, b);
   } else {
-    seq_len = lens[b];
-    total = sum_lens(lens, p.num_seqs, lane);
-    pos = sum_lens(lens, b, lane);
+    total = sum_lens(lens, p.num_seqs, lane, p.pad);
+    pos = sum_lens(lens, b, lane, p.pad);
   }
   float r0 = 0.f, r1 = 0.f;
   if (seq_len > 0) {
@@ -660,6 +657,10 @@ int ctx_decode_attn_create(const ctx_decode_attn_desc* desc, ctx_decode_attn** o
     return fail(CTX_ERR_INVALID_ARG, "unknown out_dtype %d", (int)d.out_dtype);
   if (d.split_tokens < 0 || (d.split_tokens > 0 && d.split_tokens < kBlock))
     return fail(CTX_ERR_INVALID_ARG, "split_tokens must be 0 or >= %d", kBlock);
+  if (d.page_tokens < 0 || d.page_tokens % kBlock != 0)
+    return fail(CTX_ERR_INVALID_ARG, "page_tokens must be 0 or a positive multiple of %d", kBlock);
+  if (d.page_tokens > 0 && d.split_tokens % kBlock != 0)
+    return fail(CTX_ERR_INVALID_ARG, "with page_tokens, split_tokens must be a multiple of %d", kBlock);
 
   int dev = 0;
   hipError_t e = hipGetDevice(&dev);
@@ -667,14 +668,19 @@ int ctx_decode_attn_create(const ctx_decode_attn_desc* desc, ctx_decode_attn** o
   int cus = 0;
   e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
   if (e != hipSuccess) return hip_fail(e, "hipDeviceGetAttribute");
-  int per_cu = 0;
-  if (d.out_dtype == CTX_DTYPE_F32)
-    e = hipOccupancyMaxActiveBlocksPerMultiprocessor(
-        &per_cu, reinterpret_cast<const void*>(&decode_split_kernel<float>), 64, 0);
-  else
-    e = hipOccupancyMaxActiveBlocksPerMultiprocessor(
-        &per_cu, reinterpret_cast<const void*>(&decode_split_kernel<uint16_t>), 64, 0);
-  if (e != hipSuccess) return hip_fail(e, "hipOccupancyMaxActiveBlocksPerMultiprocessor");
+  // resident single-wave workgroups per CU: the smaller of the two layouts' kernels
+  const void* kernels[2] = {
+      d.out_dtype == CTX_DTYPE_F32 ? reinterpret_cast<const void*>(&decode_split_kernel<float, false>)
+                                   : reinterpret_cast<const void*>(&decode_split_kernel<uint16_t, false>),
+      d.out_dtype == CTX_DTYPE_F32 ? reinterpret_cast<const void*>(&decode_split_kernel<float, true>)
+                                   : reinterpret_cast<const void*>(&decode_split_kernel<uint16_t, true>)};
+  int per_cu = 1 << 30;
+  for (const void* kern : kernels) {
+    int n = 0;
+    e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, kern, 64, 0);
+    if (e != hipSuccess) return hip_fail(e, "hipOccupancyMaxActiveBlocksPerMultiprocessor");
+    if (n < per_cu) per_cu = n;
+  }
   if (per_cu < 1) per_cu = 1;
 
   // one resident wave per (range, KV head); ranges in whole multiples of the XCD count
@@ -682,7 +688,8 @@ int ctx_decode_attn_create(const ctx_decode_attn_desc* desc, ctx_decode_attn** o
   if (ranges_auto < kXcds) ranges_auto = kXcds;
   int64_t max_ranges = ranges_auto;
   if (d.split_tokens > 0)
-    max_ranges = round_up(((int64_t)d.max_batch * d.max_seq_len + d.split_tokens - 1) / d.split_tokens, kXcds);
+    max_ranges = round_up(((int64_t)d.max_batch * round_up(d.max_seq_len, kBlock) + d.split_tokens - 1) /
+                              d.split_tokens, kXcds);
   if (max_ranges * d.num_kv_heads > INT32_MAX)
     return fail(CTX_ERR_INVALID_ARG, "split_tokens %d too small for max_batch x max_seq_len",
                 d.split_tokens);
@@ -710,27 +717,31 @@ int ctx_decode_attn_create(const ctx_decode_attn_desc* desc, ctx_decode_attn** o
   return CTX_OK;
 }
 
-int ctx_decode_attn_run(ctx_decode_attn* h, const void* q, const void* k_cache,
-                        const void* v_cache, const int32_t* seq_offsets, const int32_t* seq_lens,
-                        int32_t num_seqs, float scale, void* out, void* stream) {
+}  // extern "C"
+
+namespace {
+
+int check_common(ctx_decode_attn* h, int32_t num_seqs, float scale) {
   if (h == nullptr) return fail(CTX_ERR_INVALID_ARG, "handle is NULL");
   if (num_seqs < 0) return fail(CTX_ERR_INVALID_ARG, "num_seqs %d < 0", num_seqs);
   if (num_seqs > h->desc.max_batch)
     return fail(CTX_ERR_CAPACITY, "num_seqs %d > max_batch %d", num_seqs, h->desc.max_batch);
   if (!std::isfinite(scale)) return fail(CTX_ERR_INVALID_ARG, "scale is not finite");
-  if (num_seqs == 0) return CTX_OK;
-  if (q == nullptr || k_cache == nullptr || v_cache == nullptr || seq_offsets == nullptr ||
-      seq_lens == nullptr || out == nullptr)
-    return fail(CTX_ERR_INVALID_ARG, "NULL data pointer");
-  if (!aligned16(q) || !aligned16(k_cache) || !aligned16(v_cache) || !aligned16(out))
-    return fail(CTX_ERR_ALIGNMENT, "q, k_cache, v_cache and out must be 16-byte aligned");
+  return CTX_OK;
+}
+
+int check_device(ctx_decode_attn* h) {
   int dev = -1;
   hipError_t e = hipGetDevice(&dev);
   if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
   if (dev != h->device)
-    return fail(CTX_ERR_INVALID_ARG, "current device %d is not the handle's device %d", dev,
-                h->device);
+    return fail(CTX_ERR_INVALID_ARG, "current device %d is not the handle's device %d", dev, h->device);
+  return CTX_OK;
+}
 
+template <bool kPaged>
+int launch(ctx_decode_attn* h, const void* q, const void* k, const void* v, const int32_t* offs,
+           const int32_t* lens, int32_t num_seqs, float scale, void* out, void* stream, const Paged& pg) {
   const ctx_decode_attn_desc& d = h->desc;
   Plan p;
   p.num_seqs = num_seqs;
@@ -739,33 +750,85 @@ int ctx_decode_attn_run(ctx_decode_attn* h, const void* q, const void* k_cache,
   p.group = d.num_q_heads / d.num_kv_heads;
   p.forced_width = d.split_tokens;
   p.num_ranges = d.split_tokens > 0
-                     ? (int32_t)round_up(((int64_t)num_seqs * d.max_seq_len + d.split_tokens - 1) /
-                                             d.split_tokens, kXcds)
+                     ? (int32_t)round_up(((int64_t)num_seqs * round_up(d.max_seq_len, kPaged ? kBlock : 1) +
+                                          d.split_tokens - 1) / d.split_tokens, kXcds)
                      : h->ranges_auto;
+  p.pad = kPaged ? kBlock : 1;
   p.scale_log2 = (float)((double)scale * 1.4426950408889634);
 
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
   const dim3 split_grid((unsigned)(p.num_ranges * p.hkv));
   const dim3 merge_grid((unsigned)(((int64_t)num_seqs * p.hq + kMergeWaves - 1) / kMergeWaves));
   const uint16_t* qp = static_cast<const uint16_t*>(q);
-  const uint16_t* kp = static_cast<const uint16_t*>(k_cache);
-  const uint16_t* vp = static_cast<const uint16_t*>(v_cache);
+  const uint16_t* kp = static_cast<const uint16_t*>(k);
+  const uint16_t* vp = static_cast<const uint16_t*>(v);
   if (d.out_dtype == CTX_DTYPE_F32) {
     float* op = static_cast<float*>(out);
-    hipLaunchKernelGGL(decode_split_kernel<float>, split_grid, dim3(64), 0, s, qp, kp, vp,
-                       seq_offsets, seq_lens, p, h->o_ws, h->ml_ws, op);
-    hipLaunchKernelGGL(decode_merge_kernel<float>, merge_grid, dim3(64 * kMergeWaves), 0, s,
-                       seq_lens, p, h->o_ws, h->ml_ws, op);
+    hipLaunchKernelGGL((decode_split_kernel<float, kPaged>), split_grid, dim3(64), 0, s, qp, kp, vp, offs,
+                       lens, p, pg, h->o_ws, h->ml_ws, op);
+    hipLaunchKernelGGL(decode_merge_kernel<float>, merge_grid, dim3(64 * kMergeWaves), 0, s, lens, p,
+                       h->o_ws, h->ml_ws, op);
   } else {
     uint16_t* op = static_cast<uint16_t*>(out);
-    hipLaunchKernelGGL(decode_split_kernel<uint16_t>, split_grid, dim3(64), 0, s, qp, kp, vp,
-                       seq_offsets, seq_lens, p, h->o_ws, h->ml_ws, op);
-    hipLaunchKernelGGL(decode_merge_kernel<uint16_t>, merge_grid, dim3(64 * kMergeWaves), 0, s,
-                       seq_lens, p, h->o_ws, h->ml_ws, op);
+    hipLaunchKernelGGL((decode_split_kernel<uint16_t, kPaged>), split_grid, dim3(64), 0, s, qp, kp, vp,
+                       offs, lens, p, pg, h->o_ws, h->ml_ws, op);
+    hipLaunchKernelGGL(decode_merge_kernel<uint16_t>, merge_grid, dim3(64 * kMergeWaves), 0, s, lens, p,
+                       h->o_ws, h->ml_ws, op);
   }
-  e = hipGetLastError();
+  hipError_t e = hipGetLastError();
   if (e != hipSuccess) return hip_fail(e, "kernel launch");
   return CTX_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int ctx_decode_attn_run(ctx_decode_attn* h, const void* q, const void* k_cache,
+                        const void* v_cache, const int32_t* seq_offsets, const int32_t* seq_lens,
+                        int32_t num_seqs, float scale, void* out, void* stream) {
+  int rc = check_common(h, num_seqs, scale);
+  if (rc != CTX_OK || num_seqs == 0) return rc;
+  if (q == nullptr || k_cache == nullptr || v_cache == nullptr || seq_offsets == nullptr ||
+      seq_lens == nullptr || out == nullptr)
+    return fail(CTX_ERR_INVALID_ARG, "NULL data pointer");
+  if (!aligned16(q) || !aligned16(k_cache) || !aligned16(v_cache) || !aligned16(out))
+    return fail(CTX_ERR_ALIGNMENT, "q, k_cache, v_cache and out must be 16-byte aligned");
+  rc = check_device(h);
+  if (rc != CTX_OK) return rc;
+  Paged pg{};
+  return launch<false>(h, q, k_cache, v_cache, seq_offsets, seq_lens, num_seqs, scale, out, stream, pg);
+}
+
+int ctx_decode_attn_run_paged(ctx_decode_attn* h, const void* q, void* k_pages, void* v_pages,
+                              const int32_t* block_tables, int32_t max_pages_per_seq,
+                              const int32_t* seq_lens, int32_t num_seqs, const void* k_new,
+                              const void* v_new, float scale, void* out, void* stream) {
+  int rc = check_common(h, num_seqs, scale);
+  if (rc != CTX_OK) return rc;
+  if (h->desc.page_tokens <= 0)
+    return fail(CTX_ERR_UNSUPPORTED, "the handle was created without page_tokens");
+  if (num_seqs == 0) return CTX_OK;
+  if (q == nullptr || k_pages == nullptr || v_pages == nullptr || block_tables == nullptr ||
+      seq_lens == nullptr || out == nullptr)
+    return fail(CTX_ERR_INVALID_ARG, "NULL data pointer");
+  if ((k_new == nullptr) != (v_new == nullptr))
+    return fail(CTX_ERR_INVALID_ARG, "k_new and v_new must both be given or both be NULL");
+  if (max_pages_per_seq <= 0) return fail(CTX_ERR_INVALID_ARG, "max_pages_per_seq must be positive");
+  if (!aligned16(q) || !aligned16(k_pages) || !aligned16(v_pages) || !aligned16(out) ||
+      !aligned16(k_new) || !aligned16(v_new))
+    return fail(CTX_ERR_ALIGNMENT, "q, k_pages, v_pages, k_new, v_new and out must be 16-byte aligned");
+  rc = check_device(h);
+  if (rc != CTX_OK) return rc;
+  Paged pg;
+  pg.block_tables = block_tables;
+  pg.max_pages = max_pages_per_seq;
+  pg.page_tokens = h->desc.page_tokens;
+  pg.k_new = static_cast<const uint16_t*>(k_new);
+  pg.v_new = static_cast<const uint16_t*>(v_new);
+  pg.k_cache = static_cast<uint16_t*>(k_pages);
+  pg.v_cache = static_cast<uint16_t*>(v_pages);
+  return launch<true>(h, q, k_pages, v_pages, nullptr, seq_lens, num_seqs, scale, out, stream, pg);
 }
 
 int ctx_decode_attn_destroy(ctx_decode_attn* h) {

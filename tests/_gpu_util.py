@@ -89,3 +89,29 @@ class SampledLayer:
         lens = self.layout.lens_at(step)
         sl = np.array([lens[b] for b in self.sample], np.int32)
         return oracle.decode_attn(qh[self.sample], self.hk, self.hv, self.host_offsets, sl, self.w.scale)
+
+
+def paged_copy(k: np.ndarray, v: np.ndarray, lay, page_tokens: int, rng, spare_pages: int = 7,
+               fill=wl.BF16_NAN):
+    """Scatter every sequence's rows of a contiguous cache into randomly chosen
+    pages [num_pages, P, Hkv, D]; unused pages and slots hold `fill`.
+    Returns (k_pages, v_pages, block_tables) with -1 in unused table entries."""
+    caps = [int(c) for c in lay.capacity]
+    npages = [-(-c // page_tokens) for c in caps]
+    total = sum(npages) + spare_pages
+    perm = rng.permutation(total)
+    hkv, d = k.shape[1], k.shape[2]
+    kp = np.full((total, page_tokens, hkv, d), fill, np.uint16)
+    vp = np.full_like(kp, fill)
+    bt = np.full((len(caps), max(npages) + 3), -1, np.int32)
+    nxt = 0
+    for b, cap in enumerate(caps):
+        o = int(lay.offsets[b])
+        for j in range(npages[b]):
+            page = perm[nxt]
+            nxt += 1
+            bt[b, j] = page
+            n = min(page_tokens, cap - j * page_tokens)
+            kp[page, :n] = k[o + j * page_tokens: o + j * page_tokens + n]
+            vp[page, :n] = v[o + j * page_tokens: o + j * page_tokens + n]
+    return kp, vp, bt

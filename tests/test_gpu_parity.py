@@ -59,6 +59,19 @@ def test_reduced_workloads_full(name):
     assert_parity(got, ref, f"{name} reduced")
 
 
+def test_large_batch_forced_splits():
+    """More than 64 sequences (the wave-wide prefix search runs in chunks) and
+    forced split sizes that cut most sequences several times."""
+    w = wl.small_workload(wl.WORKLOADS["act_first_burst"], batch=150, lengths=(16, 700))
+    lay = wl.workload_layout(w)
+    q = wl.query_bits(w, 0)
+    k, v = wl.layer_kv_bits(w, lay, 0)
+    ref = oracle.decode_attn(q, k, v, lay.offsets, lay.lens, w.scale)
+    for split in (0, 16, 112, 1000):
+        got = run_layer(w, lay, q, k, v, split_tokens=split)
+        assert_parity(got, ref, f"B=150 split={split}")
+
+
 @pytest.mark.parametrize("name,steps", [
     ("student_0p6b_1p7b", [0]),
     ("student_4b", [0]),

@@ -330,3 +330,84 @@ def test_threads_do_not_change_results():
     pairs = np.array([[3, 15], [0, 0], [2, 7]])
     np.testing.assert_array_equal(oracle.decode_attn_pairs(q, k, v, lay.offsets, lay.lens, w.scale, pairs),
                                   a[pairs[:, 0], pairs[:, 1]])
+
+
+# ------------------------------------------------------------- paged caches
+
+def _paged_copy(k, v, lay, page_tokens, rng, spare_pages=5):
+    """Scatter every sequence's rows into randomly chosen pages; unused slots
+    and pages hold NaN.  Returns pages and block tables."""
+    caps = [int(c) for c in lay.capacity]
+    npages_seq = [-(-c // page_tokens) for c in caps]
+    total = sum(npages_seq) + spare_pages
+    perm = rng.permutation(total)
+    hkv, d = k.shape[1], k.shape[2]
+    kp = np.full((total, page_tokens, hkv, d), wl.BF16_NAN, np.uint16)
+    vp = np.full_like(kp, wl.BF16_NAN)
+    bt = np.full((len(caps), max(npages_seq) + 2), -1, np.int32)
+    nxt = 0
+    for b, cap in enumerate(caps):
+        o = int(lay.offsets[b])
+        for j in range(npages_seq[b]):
+            page = perm[nxt]
+            nxt += 1
+            bt[b, j] = page
+            n = min(page_tokens, cap - j * page_tokens)
+            kp[page, :n] = k[o + j * page_tokens: o + j * page_tokens + n]
+            vp[page, :n] = v[o + j * page_tokens: o + j * page_tokens + n]
+    return kp, vp, bt
+
+
+@pytest.mark.parametrize("page_tokens", [16, 32, 48])
+def test_paged_oracle_equals_contiguous(page_tokens):
+    """The block-table indirection changes where rows live, not what is
+    computed: scattered pages with NaN everywhere else give exactly the
+    contiguous oracle's output."""
+    rng = np.random.default_rng(31 + page_tokens)
+    w = wl.Workload("pg", 91, 1, 7, 16, 4, 3, "uniform", 1, 200)
+    lens = wl.draw_lengths(w)
+    lens[:3] = [1, page_tokens, page_tokens + 1]
+    lay = wl.make_layout(lens, steps=3)
+    k, v = wl.layer_kv_bits(w, lay, 0)
+    q = wl.query_bits(w, 0)
+    ref = oracle.decode_attn(q, k, v, lay.offsets, lens, w.scale)
+    kp, vp, bt = _paged_copy(k, v, lay, page_tokens, rng)
+    got = oracle.decode_attn_paged(q, kp, vp, bt, lens, w.scale)
+    np.testing.assert_array_equal(got, ref)
+
+
+def test_paged_append_uses_the_new_token():
+    """With k_new / v_new the newest token's cache slot is ignored (it holds NaN
+    here) and the new rows are attended instead: identical to the contiguous
+    oracle on a cache where that row was written."""
+    rng = np.random.default_rng(41)
+    w = wl.Workload("pa", 92, 1, 6, 8, 2, 1, "uniform", 1, 90)
+    lens = wl.draw_lengths(w)
+    lens[0] = 1
+    lay = wl.make_layout(lens, steps=1)
+    k, v = wl.layer_kv_bits(w, lay, 0)
+    q = wl.query_bits(w, 0)
+    k_new = rand_bits(rng, (6, 2, 128))
+    v_new = rand_bits(rng, (6, 2, 128))
+    k2, v2 = k.copy(), v.copy()
+    for b in range(6):
+        r = lay.offsets[b] + lens[b] - 1
+        k2[r], v2[r] = k_new[b], v_new[b]
+        k[r] = wl.BF16_NAN
+        v[r] = wl.BF16_NAN
+    ref = oracle.decode_attn(q, k2, v2, lay.offsets, lens, w.scale)
+    kp, vp, bt = _paged_copy(k, v, lay, 16, rng)
+    got = oracle.decode_attn_paged(q, kp, vp, bt, lens, w.scale, k_new, v_new)
+    np.testing.assert_array_equal(got, ref)
+    # without the append the NaN slot is read
+    assert np.isnan(oracle.decode_attn_paged(q, kp, vp, bt, lens, w.scale)).any()
+
+
+def test_paged_rejects_bad_block_tables():
+    rng = np.random.default_rng(42)
+    kp = rand_bits(rng, (3, 16, 1, 128))
+    q = rand_bits(rng, (1, 1, 128))
+    with pytest.raises(ValueError):
+        oracle.decode_attn_paged(q, kp, kp, np.array([[0, 7]], np.int32), [20], 0.1)
+    with pytest.raises(ValueError):
+        oracle.decode_attn_paged(q, kp, kp, np.array([[0]], np.int32), [20], 0.1)
