@@ -33,6 +33,8 @@ def _load():
         lib.oracle_decode_attn_paged_pairs.argtypes = [p, p, p, p, i32, i32, i64, p, i32, i32, i32, i32,
                                                        f64, p, p, p, i64, p, i32]
         lib.oracle_decode_attn_paged_pairs.restype = ctypes.c_int
+        lib.oracle_prefill_attn.argtypes = [p, p, p, p, p, p, p, i32, i32, i32, i32, i64, i64, f64, p, i32]
+        lib.oracle_prefill_attn.restype = ctypes.c_int
         _lib = lib
     return _lib
 
@@ -125,3 +127,18 @@ def decode_attn_paged(q, k_pages, v_pages, block_tables, seq_lens, scale, k_new=
         d, float(scale), _ptr(kn) if kn is not None else nullp, _ptr(vn) if vn is not None else nullp,
         _ptr(pairs), len(pairs), _ptr(out), threads))
     return out.reshape(shape) if shape is not None else out
+
+
+def prefill_attn(q, k, v, seq_offsets, seq_lens, q_starts, q_lens, scale, threads: int = 0) -> np.ndarray:
+    """Causal prefill: q [total_q, Hq, D]; sequence b's q_lens[b] queries (rows
+    q_starts[b] ..) are its last q_lens[b] tokens; returns float64 [total_q, Hq, D]
+    (rows of no sequence stay 0)."""
+    q, k, v = _u16(q), _u16(k), _u16(v)
+    offs, lens = _i32(seq_offsets), _i32(seq_lens)
+    qs, ql = _i32(q_starts), _i32(q_lens)
+    total_q, hq, d = q.shape
+    rows, hkv, _ = k.shape
+    out = np.zeros((total_q, hq, d), dtype=np.float64)
+    _check(_load().oracle_prefill_attn(_ptr(q), _ptr(k), _ptr(v), _ptr(offs), _ptr(lens), _ptr(qs), _ptr(ql),
+                                       len(lens), hq, hkv, d, rows, total_q, float(scale), _ptr(out), threads))
+    return out

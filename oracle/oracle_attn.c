@@ -73,24 +73,18 @@ static int check_shape(int32_t num_seqs, int32_t hq, int32_t hkv, int32_t d)
 }
 
 /*
- * Attention weights w_t of one (sequence, query head): the softmax of the
- * scaled logits over the sequence's rows.  Writes L_b doubles to w.
+ * Attention weights w_t of one query row over len consecutive cache rows
+ * starting at row off, KV head kv: the softmax of the scaled logits.
+ * Writes len doubles to w.
  */
-static int weights_one(const uint16_t *q, const uint16_t *k,
-                       const int32_t *seq_offsets, const int32_t *seq_lens,
-                       int32_t b, int32_t h, int32_t hq, int32_t hkv, int32_t d,
-                       int64_t num_rows, double scale, double *w)
+static int weights_rows(const uint16_t *qrow, const uint16_t *k, int64_t off, int64_t len,
+                        int32_t kv, int32_t hkv, int32_t d, int64_t num_rows, double scale,
+                        double *w)
 {
-    const int32_t g = hq / hkv;
-    const int32_t kv = h / g;
-    const int64_t off = seq_offsets[b];
-    const int64_t len = seq_lens[b];
     if (len < 0 || off < 0 || off + len > num_rows)
         return ORACLE_ERR_RANGE;
     if (len == 0)
         return ORACLE_OK;
-
-    const uint16_t *qrow = q + ((int64_t)b * hq + h) * d;
     double smax = -INFINITY;
     for (int64_t t = 0; t < len; ++t) {
         const uint16_t *krow = k + ((off + t) * hkv + kv) * d;
@@ -111,26 +105,41 @@ static int weights_one(const uint16_t *q, const uint16_t *k,
     return ORACLE_OK;
 }
 
-/* out[d] = sum_t w_t V[r_t, kv, :] for one (sequence, query head). */
-static int attend_one(const uint16_t *q, const uint16_t *k, const uint16_t *v,
-                      const int32_t *seq_offsets, const int32_t *seq_lens,
-                      int32_t b, int32_t h, int32_t hq, int32_t hkv, int32_t d,
-                      int64_t num_rows, double scale, double *w, double *out)
+/* out[:] = sum_t w_t V[off + t, kv, :] for one query row. */
+static int attend_rows(const uint16_t *qrow, const uint16_t *k, const uint16_t *v, int64_t off,
+                       int64_t len, int32_t kv, int32_t hkv, int32_t d, int64_t num_rows,
+                       double scale, double *w, double *out)
 {
-    const int32_t kv = h / (hq / hkv);
     for (int32_t i = 0; i < d; ++i)
         out[i] = 0.0;
-    int rc = weights_one(q, k, seq_offsets, seq_lens, b, h, hq, hkv, d, num_rows, scale, w);
+    int rc = weights_rows(qrow, k, off, len, kv, hkv, d, num_rows, scale, w);
     if (rc != ORACLE_OK)
         return rc;
-    const int64_t off = seq_offsets[b];
-    const int64_t len = seq_lens[b];
     for (int64_t t = 0; t < len; ++t) {
         const uint16_t *vrow = v + ((off + t) * hkv + kv) * d;
         for (int32_t i = 0; i < d; ++i)
             out[i] += w[t] * bf16_value(vrow[i]);
     }
     return ORACLE_OK;
+}
+
+/* Decode: the one new query of sequence b, query head h, over the sequence's rows. */
+static int weights_one(const uint16_t *q, const uint16_t *k,
+                       const int32_t *seq_offsets, const int32_t *seq_lens,
+                       int32_t b, int32_t h, int32_t hq, int32_t hkv, int32_t d,
+                       int64_t num_rows, double scale, double *w)
+{
+    return weights_rows(q + ((int64_t)b * hq + h) * d, k, seq_offsets[b], seq_lens[b],
+                        h / (hq / hkv), hkv, d, num_rows, scale, w);
+}
+
+static int attend_one(const uint16_t *q, const uint16_t *k, const uint16_t *v,
+                      const int32_t *seq_offsets, const int32_t *seq_lens,
+                      int32_t b, int32_t h, int32_t hq, int32_t hkv, int32_t d,
+                      int64_t num_rows, double scale, double *w, double *out)
+{
+    return attend_rows(q + ((int64_t)b * hq + h) * d, k, v, seq_offsets[b], seq_lens[b],
+                       h / (hq / hkv), hkv, d, num_rows, scale, w, out);
 }
 
 static int64_t max_len(const int32_t *seq_lens, int32_t n)
@@ -362,5 +371,88 @@ int oracle_decode_attn_paged_pairs(const uint16_t *q, const uint16_t *k_pages, c
         }
         free(w);
     }
+    return status;
+}
+
+/* ---------------------------------------------------------------- prefill */
+
+/*
+ * Causal prefill of the newest tokens of each sequence against its cache:
+ * the reference-conditioned fast action first adds the reference next
+ * observation o^ref_{t+1} to the context (Sec. 4.1,
+ * eq:reference-conditioned-action), chunked-prefilled by the serving engine
+ * (tab:scheduling-hyperparameters: chunked prefill on).  Sequence b has
+ * L_b = seq_lens[b] cached rows from seq_offsets[b], the last n_b = q_lens[b]
+ * of which are the new tokens; their queries are rows q_starts[b] + i of q
+ * [total_q, Hq, D].  Query i sits at position p = L_b - n_b + i and attends
+ * to positions 0 .. p, so its output is exactly the decode result over the
+ * first p + 1 rows of the sequence.  out has q's layout (double).
+ */
+int oracle_prefill_attn(const uint16_t *q, const uint16_t *k, const uint16_t *v,
+                        const int32_t *seq_offsets, const int32_t *seq_lens,
+                        const int32_t *q_starts, const int32_t *q_lens, int32_t num_seqs,
+                        int32_t hq, int32_t hkv, int32_t d, int64_t num_rows, int64_t total_q,
+                        double scale, double *out, int32_t num_threads)
+{
+    int rc = check_shape(num_seqs, hq, hkv, d);
+    if (rc != ORACLE_OK)
+        return rc;
+    int64_t jobs = 0;
+    for (int32_t b = 0; b < num_seqs; ++b) {
+        if (q_lens[b] < 0 || q_lens[b] > seq_lens[b] || q_starts[b] < 0 ||
+            (int64_t)q_starts[b] + q_lens[b] > total_q)
+            return ORACLE_ERR_ARG;
+        jobs += q_lens[b];
+    }
+    int64_t *row_seq = (int64_t *)malloc((size_t)(jobs > 0 ? jobs : 1) * 2 * sizeof(int64_t));
+    if (row_seq == NULL)
+        return ORACLE_ERR_NOMEM;
+    int64_t j = 0;
+    for (int32_t b = 0; b < num_seqs; ++b)
+        for (int32_t i = 0; i < q_lens[b]; ++i) {
+            row_seq[2 * j] = b;
+            row_seq[2 * j + 1] = i;
+            ++j;
+        }
+    const int64_t lmax = max_len(seq_lens, num_seqs);
+    int status = ORACLE_OK;
+#ifdef _OPENMP
+    if (num_threads <= 0)
+        num_threads = omp_get_max_threads();
+#pragma omp parallel num_threads(num_threads)
+#endif
+    {
+        double *w = (double *)malloc((size_t)(lmax > 0 ? lmax : 1) * sizeof(double));
+        if (w == NULL) {
+#ifdef _OPENMP
+#pragma omp atomic write
+#endif
+            status = ORACLE_ERR_NOMEM;
+        }
+#ifdef _OPENMP
+#pragma omp for schedule(dynamic, 1)
+#endif
+        for (int64_t r = 0; r < jobs; ++r) {
+            if (w == NULL)
+                continue;
+            const int32_t b = (int32_t)row_seq[2 * r];
+            const int32_t i = (int32_t)row_seq[2 * r + 1];
+            const int64_t pos = (int64_t)seq_lens[b] - q_lens[b] + i;
+            const int64_t qrow = (int64_t)q_starts[b] + i;
+            for (int32_t h = 0; h < hq; ++h) {
+                int e = attend_rows(q + (qrow * hq + h) * d, k, v, seq_offsets[b], pos + 1,
+                                    h / (hq / hkv), hkv, d, num_rows, scale, w,
+                                    out + (qrow * hq + h) * d);
+                if (e != ORACLE_OK) {
+#ifdef _OPENMP
+#pragma omp atomic write
+#endif
+                    status = e;
+                }
+            }
+        }
+        free(w);
+    }
+    free(row_seq);
     return status;
 }

@@ -411,3 +411,58 @@ def test_paged_rejects_bad_block_tables():
         oracle.decode_attn_paged(q, kp, kp, np.array([[0, 7]], np.int32), [20], 0.1)
     with pytest.raises(ValueError):
         oracle.decode_attn_paged(q, kp, kp, np.array([[0]], np.int32), [20], 0.1)
+
+
+# ------------------------------------------------------------- causal prefill
+
+def test_prefill_rows_are_decodes_of_growing_prefixes():
+    """Query i of a sequence with L rows and n new tokens is the decode of the
+    first L - n + i + 1 rows: checked against the pinned decode path, with
+    sequences and query rows in shuffled places."""
+    rng = np.random.default_rng(61)
+    hq, hkv, d = 8, 2, 128
+    lens = np.array([1, 20, 33, 7], np.int32)
+    qlen = np.array([1, 5, 33, 0], np.int32)
+    lay = wl.make_layout(lens, 1, gap_max=3, shuffle=True, rng=rng)
+    k = rand_bits(rng, (lay.num_rows, hkv, d))
+    v = rand_bits(rng, (lay.num_rows, hkv, d))
+    q_starts = np.array([40, 0, 6, 39], np.int32)
+    q = rand_bits(rng, (80, hq, d))
+    out = oracle.prefill_attn(q, k, v, lay.offsets, lens, q_starts, qlen, 0.09)
+    for b in range(4):
+        for i in range(qlen[b]):
+            row = q_starts[b] + i
+            dec = oracle.decode_attn(q[row:row + 1], k, v, [lay.offsets[b]], [lens[b] - qlen[b] + i + 1], 0.09)
+            np.testing.assert_array_equal(out[row], dec[0])
+    untouched = np.ones(80, bool)
+    for b in range(4):
+        untouched[q_starts[b]:q_starts[b] + qlen[b]] = False
+    assert (out[untouched] == 0).all()
+
+
+def test_prefill_is_causal():
+    """Changing a later token's K/V never changes an earlier query's output;
+    the first new query of a fresh sequence (L = n) sees only itself."""
+    rng = np.random.default_rng(62)
+    L = 24
+    k = rand_bits(rng, (L, 1, 128))
+    v = rand_bits(rng, (L, 1, 128))
+    q = rand_bits(rng, (L, 2, 128))
+    a = oracle.prefill_attn(q, k, v, [0], [L], [0], [L], 0.1)
+    k2, v2 = k.copy(), v.copy()
+    k2[15:] = rand_bits(rng, (L - 15, 1, 128))
+    v2[15:] = rand_bits(rng, (L - 15, 1, 128))
+    b = oracle.prefill_attn(q, k2, v2, [0], [L], [0], [L], 0.1)
+    np.testing.assert_array_equal(a[:15], b[:15])
+    assert not np.array_equal(a[15:], b[15:])
+    np.testing.assert_array_equal(a[0, 0], unbf(v[0, 0]).astype(np.float64))
+
+
+def test_prefill_rejects_bad_lengths():
+    rng = np.random.default_rng(63)
+    k = rand_bits(rng, (8, 1, 128))
+    q = rand_bits(rng, (4, 1, 128))
+    with pytest.raises(ValueError):
+        oracle.prefill_attn(q, k, k, [0], [3], [0], [4], 0.1)   # more queries than tokens
+    with pytest.raises(ValueError):
+        oracle.prefill_attn(q, k, k, [0], [8], [2], [3], 0.1)   # query rows past q
