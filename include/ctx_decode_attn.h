@@ -145,6 +145,35 @@ int ctx_decode_attn_run_paged(ctx_decode_attn* handle, const void* q, void* k_pa
                               const int32_t* seq_lens, int32_t num_seqs, const void* k_new,
                               const void* v_new, float scale, void* out, void* stream);
 
+/*
+ * Causal prefill of each sequence's newest tokens against its cache.  The
+ * reference-conditioned fast action adds the reference next observation
+ * o^ref_{t+1} to the context before decoding (Sec. 4.1,
+ * eq:reference-conditioned-action); the serving engine prefills such tokens
+ * in chunks (tab:scheduling-hyperparameters).  Query i of sequence b sits at
+ * position p = seq_lens[b] - q_lens[b] + i and attends to positions 0 .. p:
+ *
+ *   out[q_starts[b] + i, h, :] = sum_{t <= p} softmax_t(scale q.K[r_t, kv]) V[r_t, kv, :]
+ *
+ * with r_t = seq_offsets[b] + t and kv = h / (Hq / Hkv).
+ *   q            bf16 [total_q, Hq, D]: sequence b's queries are rows q_starts[b] ..
+ *                q_starts[b] + q_lens[b] - 1 (any order, no overlap)
+ *   k_cache, v_cache  bf16 [R, Hkv, D] as in ctx_decode_attn_run; they already hold
+ *                the new tokens' rows (the last q_lens[b] of the sequence)
+ *   seq_offsets, seq_lens  int32 [num_seqs] as in ctx_decode_attn_run
+ *   q_starts, q_lens  int32 [num_seqs]; 0 <= q_lens[b] <= seq_lens[b] and
+ *                q_lens[b] <= max_q_len (device contract: undefined otherwise)
+ *   max_q_len    host bound on q_lens (sizes the grid)
+ *   out          [total_q, Hq, D] of desc.out_dtype; rows of no sequence are untouched
+ * Needs a group size Hq / Hkv dividing 16 (UNSUPPORTED otherwise).  No
+ * workspace, no allocation, no host sync; deterministic.
+ * Errors: INVALID_ARG, UNSUPPORTED, CAPACITY, ALIGNMENT, HIP.
+ */
+int ctx_prefill_attn_run(ctx_decode_attn* handle, const void* q, const void* k_cache, const void* v_cache,
+                         const int32_t* seq_offsets, const int32_t* seq_lens, const int32_t* q_starts,
+                         const int32_t* q_lens, int32_t num_seqs, int32_t max_q_len, float scale,
+                         void* out, void* stream);
+
 /* Wait for the handle's device, free the workspace and the handle.  NULL is a no-op. */
 int ctx_decode_attn_destroy(ctx_decode_attn* handle);
 

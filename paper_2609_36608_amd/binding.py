@@ -27,6 +27,7 @@ EXPORTS = (
     "ctx_decode_attn_create",
     "ctx_decode_attn_run",
     "ctx_decode_attn_run_paged",
+    "ctx_prefill_attn_run",
     "ctx_decode_attn_destroy",
     "ctx_decode_attn_status_string",
     "ctx_decode_attn_last_error",
@@ -75,6 +76,8 @@ def load_library(path: str | None = None):
     lib.ctx_decode_attn_run.restype = ctypes.c_int
     lib.ctx_decode_attn_run_paged.argtypes = [vp, vp, vp, vp, vp, i32, vp, i32, vp, vp, ctypes.c_float, vp, vp]
     lib.ctx_decode_attn_run_paged.restype = ctypes.c_int
+    lib.ctx_prefill_attn_run.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp, i32, i32, ctypes.c_float, vp, vp]
+    lib.ctx_prefill_attn_run.restype = ctypes.c_int
     lib.ctx_decode_attn_destroy.argtypes = [vp]
     lib.ctx_decode_attn_destroy.restype = ctypes.c_int
     lib.ctx_decode_attn_status_string.argtypes = [ctypes.c_int]
@@ -195,6 +198,42 @@ class DecodeAttention:
             block_tables.shape[1], seq_lens.data_ptr(), b,
             k_new.data_ptr() if k_new is not None else None, v_new.data_ptr() if v_new is not None else None,
             float(scale), out.data_ptr(), sp)
+        if rc != CTX_OK:
+            raise error_for(self.lib, rc)
+        return out
+
+    def prefill(self, q, k_cache, v_cache, seq_offsets, seq_lens, q_starts, q_lens, max_q_len: int,
+                scale: float, out, stream=None):
+        """Causal prefill: q / out [total_q, Hq, D]; sequence b's q_lens[b] queries
+        (rows q_starts[b] ..) are the last q_lens[b] of its seq_lens[b] cached rows."""
+        import torch
+
+        if self.handle is None:
+            raise RuntimeError("handle is closed")
+        d = self.desc
+        for name, t, dt in (("q", q, torch.bfloat16), ("k_cache", k_cache, torch.bfloat16),
+                            ("v_cache", v_cache, torch.bfloat16), ("seq_offsets", seq_offsets, torch.int32),
+                            ("seq_lens", seq_lens, torch.int32), ("q_starts", q_starts, torch.int32),
+                            ("q_lens", q_lens, torch.int32), ("out", out, self.out_dtype)):
+            if t.dtype != dt:
+                raise TypeError(f"{name} must be {dt}, got {t.dtype}")
+            if not t.is_cuda or t.device.index != self.device:
+                raise ValueError(f"{name} must be on cuda:{self.device}")
+            if not t.is_contiguous():
+                raise ValueError(f"{name} must be contiguous")
+        b = seq_lens.shape[0]
+        if q.dim() != 3 or q.shape[1:] != (d.num_q_heads, d.head_dim) or out.shape != q.shape:
+            raise ValueError(f"q/out must be [rows, {d.num_q_heads}, {d.head_dim}]")
+        if k_cache.dim() != 3 or k_cache.shape[1:] != (d.num_kv_heads, d.head_dim) or v_cache.shape != k_cache.shape:
+            raise ValueError(f"k_cache/v_cache must be [rows, {d.num_kv_heads}, {d.head_dim}]")
+        if seq_offsets.shape != (b,) or q_starts.shape != (b,) or q_lens.shape != (b,):
+            raise ValueError(f"seq_offsets, seq_lens, q_starts, q_lens must all be [{b}]")
+        if stream is None:
+            stream = torch.cuda.current_stream()
+        sp = stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream)
+        rc = self.lib.ctx_prefill_attn_run(self.handle, q.data_ptr(), k_cache.data_ptr(), v_cache.data_ptr(),
+                                           seq_offsets.data_ptr(), seq_lens.data_ptr(), q_starts.data_ptr(),
+                                           q_lens.data_ptr(), b, int(max_q_len), float(scale), out.data_ptr(), sp)
         if rc != CTX_OK:
             raise error_for(self.lib, rc)
         return out

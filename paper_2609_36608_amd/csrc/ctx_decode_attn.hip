@@ -585,6 +585,199 @@ __global__ __launch_bounds__(64 * kMergeWaves) void decode_merge_kernel(
   store2<OutT>(out + ((size_t)b * p.hq + h) * kHeadDim + 2 * lane, r0, r1);
 }
 
+// ------------------------------------------------------------ prefill kernel
+//
+// Causal prefill of each sequence's newest tokens (the reference next
+// observation the fast action conditions on) against its cache, which already
+// holds their K/V rows.  Query column n of a 16-column MFMA tile is query
+// position n / g, head n % g of one KV group (g divides 16), so every column
+// carries work.  A workgroup of kPrefillWaves waves covers kPrefillCols
+// columns of one (sequence, KV head); the waves share each 16-token K/V block
+// through a double-buffered LDS tile and stream the blocks up to the
+// workgroup's last query position.  The per-block math is the decode
+// kernel's: V transposed by a selector MFMA once per block, then for each of
+// the wave's column tiles S^T = K Q^T, the causal mask, the lazy online
+// softmax and O^T += V^T (P_hi + P_lo)^T.
+
+constexpr int kPrefillWaves = 4;
+constexpr int kPrefillTiles = 2;  // 16-column tiles per wave
+constexpr int kPrefillCols = kPrefillWaves * kPrefillTiles * 16;
+
+struct PrefillPlan {
+  int32_t hq;
+  int32_t hkv;
+  int32_t group;
+  int32_t tiles;  // workgroups per (sequence, KV head)
+  float scale_log2;
+};
+
+template <typename OutT>
+__global__ __launch_bounds__(64 * kPrefillWaves) void prefill_kernel(
+    const uint16_t* __restrict__ q, const uint16_t* __restrict__ kc, const uint16_t* __restrict__ vc,
+    const int32_t* __restrict__ offs, const int32_t* __restrict__ lens,
+    const int32_t* __restrict__ q_starts, const int32_t* __restrict__ q_lens, PrefillPlan pp,
+    OutT* __restrict__ out) {
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = tid >> 6;
+  const int n = lane & 15;
+  const int c = lane >> 4;
+  const int g = pp.group;
+  const int tile = blockIdx.x % pp.tiles;
+  const int unit = blockIdx.x / pp.tiles;
+  const int kv = unit % pp.hkv;
+  const int b = unit / pp.hkv;
+  const int nq = q_lens[b];
+  const int first_q = tile * (kPrefillCols / g);
+  if (first_q >= nq) return;  // the whole workgroup: nothing to do
+  const int seq_len = lens[b];
+  const int last_q = (first_q + kPrefillCols / g < nq ? first_q + kPrefillCols / g : nq) - 1;
+  const int kv_end = seq_len - nq + last_q + 1;  // tokens any query of the workgroup attends to
+  const size_t row_elems = (size_t)pp.hkv * kHeadDim;
+  const int row_bytes = (int)(row_elems * 2);
+  const uint16_t* kseq = kc + (size_t)offs[b] * row_elems + (size_t)kv * kHeadDim;
+  const uint16_t* vseq = vc + (size_t)offs[b] * row_elems + (size_t)kv * kHeadDim;
+
+  __shared__ __attribute__((aligned(16))) uint16_t lds_k[2][kBlock * kHeadDim];
+  __shared__ __attribute__((aligned(16))) uint16_t lds_v[2][kBlock * kHeadDim];
+
+  // this lane's query column in each tile: query index qi, head kv * g + hh,
+  // attending to positions 0 .. last_pos (columns past the last query attend
+  // to the whole block range and are not written)
+  int qi[kPrefillTiles], hh[kPrefillTiles], last_pos[kPrefillTiles];
+  bf16x8 qb[kPrefillTiles][4];
+#pragma unroll
+  for (int ct = 0; ct < kPrefillTiles; ++ct) {
+    const int col = tile * kPrefillCols + (wave * kPrefillTiles + ct) * 16 + n;
+    qi[ct] = col / g;
+    hh[ct] = col - qi[ct] * g;
+    const bool valid = qi[ct] < nq;
+    last_pos[ct] = valid ? seq_len - nq + qi[ct] : kv_end - 1;
+    if (valid) {
+      const uint16_t* qrow =
+          q + ((size_t)(q_starts[b] + qi[ct]) * pp.hq + (size_t)kv * g + hh[ct]) * kHeadDim + 8 * c;
+#pragma unroll
+      for (int kk = 0; kk < 4; ++kk) qb[ct][kk] = as_bf16x8(load16(qrow + 32 * kk));
+    } else {
+#pragma unroll
+      for (int kk = 0; kk < 4; ++kk) qb[ct][kk] = as_bf16x8(u32x4{0u, 0u, 0u, 0u});
+    }
+  }
+  bf16x8 sel[2];
+#pragma unroll
+  for (int h = 0; h < 2; ++h)
+#pragma unroll
+    for (int j = 0; j < 8; ++j) sel[h][j] = (8 * c + j == 16 * h + n) ? (__bf16)1.0f : (__bf16)0.0f;
+
+  Softmax st[kPrefillTiles];
+  f32x4 o[kPrefillTiles][8];
+#pragma unroll
+  for (int ct = 0; ct < kPrefillTiles; ++ct) {
+    st[ct] = Softmax{-INFINITY, 0.f};
+#pragma unroll
+    for (int nb = 0; nb < 8; ++nb) o[ct][nb] = f32x4{0.f, 0.f, 0.f, 0.f};
+  }
+
+  // cooperative block loads: thread tid fetches 16 bytes (chunk tid % 16) of
+  // token tid / 16 of K and of V; past kv_end the buffer bound returns zeros
+  const int ld_tok = tid >> 4;
+  const int ld_slot = ld_tok * kHeadDim + (((tid & 15) ^ ld_tok) << 3);
+  const int voff = ld_tok * row_bytes + (tid & 15) * 16;
+  u32x4 pk, pv;
+  {
+    const uint32_t bytes = (uint32_t)((kv_end < kBlock ? kv_end : kBlock) * row_bytes);
+    pk = buf_load16(make_rsrc(kseq, bytes), voff, 0);
+    pv = buf_load16(make_rsrc(vseq, bytes), voff, 0);
+    *reinterpret_cast<u32x4*>(&lds_k[0][ld_slot]) = pk;
+    *reinterpret_cast<u32x4*>(&lds_v[0][ld_slot]) = pv;
+  }
+  __syncthreads();
+  int buf = 0;
+  for (int t0 = 0; t0 < kv_end; t0 += kBlock) {
+    const bool more = t0 + kBlock < kv_end;
+    if (more) {  // next block in flight during this one's math
+      const int rem = kv_end - t0 - kBlock;
+      const uint32_t bytes = (uint32_t)((rem < kBlock ? rem : kBlock) * row_bytes);
+      pk = buf_load16(make_rsrc(kseq + (size_t)(t0 + kBlock) * row_elems, bytes), voff, 0);
+      pv = buf_load16(make_rsrc(vseq + (size_t)(t0 + kBlock) * row_elems, bytes), voff, 0);
+    }
+    u32x4 kr[4], vr[4];
+#pragma unroll
+    for (int kk = 0; kk < 4; ++kk) {
+      const int slot = n * kHeadDim + (((4 * kk + c) ^ n) << 3);
+      kr[kk] = *reinterpret_cast<const u32x4*>(&lds_k[buf][slot]);
+      vr[kk] = *reinterpret_cast<const u32x4*>(&lds_v[buf][slot]);
+    }
+    // V^T operands: lane (c, n) of nb holds V[token 4c+i][dim 16 nb + n]
+    s16x4 vt[8];
+    const f32x4 zero = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int kk = 0; kk < 4; ++kk)
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        const f32x4 t = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(vr[kk]), sel[h], zero, 0, 0, 0);
+        vt[2 * kk + h] = pack_bf16x4(t[0], t[1], t[2], t[3]);
+      }
+#pragma unroll
+    for (int ct = 0; ct < kPrefillTiles; ++ct) {
+      f32x4 s = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int kk = 0; kk < 4; ++kk)
+        s = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(kr[kk]), qb[ct][kk], s, 0, 0, 0);
+      float x[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        x[i] = s[i] * pp.scale_log2;
+        if (t0 + 4 * c + i > last_pos[ct]) x[i] = -INFINITY;  // causal (and past kv_end)
+      }
+      float mx = fmaxf(fmaxf(x[0], x[1]), fmaxf(x[2], x[3]));
+      mx = fmaxf(mx, __shfl_xor(mx, 16));
+      mx = fmaxf(mx, __shfl_xor(mx, 32));
+      if (__any(mx > st[ct].m + kLazyRescale)) {
+        const float m_new = fmaxf(st[ct].m, mx);
+        const float alpha = fast_exp2(st[ct].m - m_new);
+        st[ct].l *= alpha;
+#pragma unroll
+        for (int nb = 0; nb < 8; ++nb) o[ct][nb] *= alpha;
+        st[ct].m = m_new;
+      }
+      float pr[4], hi[4], lo[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        pr[i] = fast_exp2(x[i] - st[ct].m);
+        hi[i] = (float)(__bf16)pr[i];
+        lo[i] = pr[i] - hi[i];
+      }
+      st[ct].l += (pr[0] + pr[1]) + (pr[2] + pr[3]);
+      const s16x4 p_hi = pack_bf16x4(hi[0], hi[1], hi[2], hi[3]);
+      const s16x4 p_lo = pack_bf16x4(lo[0], lo[1], lo[2], lo[3]);
+#pragma unroll
+      for (int nb = 0; nb < 8; ++nb) {
+        o[ct][nb] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(vt[nb], p_hi, o[ct][nb], 0, 0, 0);
+        o[ct][nb] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(vt[nb], p_lo, o[ct][nb], 0, 0, 0);
+      }
+    }
+    if (more) {  // the other buffer was released at the previous barrier
+      *reinterpret_cast<u32x4*>(&lds_k[buf ^ 1][ld_slot]) = pk;
+      *reinterpret_cast<u32x4*>(&lds_v[buf ^ 1][ld_slot]) = pv;
+    }
+    __syncthreads();
+    buf ^= 1;
+  }
+
+#pragma unroll
+  for (int ct = 0; ct < kPrefillTiles; ++ct) {
+    float l_tot = st[ct].l + __shfl_xor(st[ct].l, 16);
+    l_tot += __shfl_xor(l_tot, 32);
+    if (qi[ct] < nq) {
+      const float inv = 1.0f / l_tot;
+      OutT* orow = out + ((size_t)(q_starts[b] + qi[ct]) * pp.hq + (size_t)kv * g + hh[ct]) * kHeadDim + 4 * c;
+#pragma unroll
+      for (int nb = 0; nb < 8; ++nb) store4<OutT>(orow + 16 * nb, o[ct][nb] * inv);
+    }
+  }
+}
+
 // ------------------------------------------------------------ host side
 
 thread_local char g_last_error[512] = "";
@@ -829,6 +1022,48 @@ int ctx_decode_attn_run_paged(ctx_decode_attn* h, const void* q, void* k_pages, 
   pg.k_cache = static_cast<uint16_t*>(k_pages);
   pg.v_cache = static_cast<uint16_t*>(v_pages);
   return launch<true>(h, q, k_pages, v_pages, nullptr, seq_lens, num_seqs, scale, out, stream, pg);
+}
+
+int ctx_prefill_attn_run(ctx_decode_attn* h, const void* q, const void* k_cache, const void* v_cache,
+                         const int32_t* seq_offsets, const int32_t* seq_lens, const int32_t* q_starts,
+                         const int32_t* q_lens, int32_t num_seqs, int32_t max_q_len, float scale,
+                         void* out, void* stream) {
+  int rc = check_common(h, num_seqs, scale);
+  if (rc != CTX_OK) return rc;
+  const ctx_decode_attn_desc& d = h->desc;
+  const int g = d.num_q_heads / d.num_kv_heads;
+  if (16 % g != 0)
+    return fail(CTX_ERR_UNSUPPORTED, "prefill needs a group size dividing 16 (got %d)", g);
+  if (max_q_len < 0) return fail(CTX_ERR_INVALID_ARG, "max_q_len %d < 0", max_q_len);
+  if (num_seqs == 0 || max_q_len == 0) return CTX_OK;
+  if (q == nullptr || k_cache == nullptr || v_cache == nullptr || seq_offsets == nullptr ||
+      seq_lens == nullptr || q_starts == nullptr || q_lens == nullptr || out == nullptr)
+    return fail(CTX_ERR_INVALID_ARG, "NULL data pointer");
+  if (!aligned16(q) || !aligned16(k_cache) || !aligned16(v_cache) || !aligned16(out))
+    return fail(CTX_ERR_ALIGNMENT, "q, k_cache, v_cache and out must be 16-byte aligned");
+  rc = check_device(h);
+  if (rc != CTX_OK) return rc;
+  PrefillPlan pp;
+  pp.hq = d.num_q_heads;
+  pp.hkv = d.num_kv_heads;
+  pp.group = g;
+  pp.tiles = (int32_t)(((int64_t)max_q_len * g + kPrefillCols - 1) / kPrefillCols);
+  pp.scale_log2 = (float)((double)scale * 1.4426950408889634);
+  const int64_t blocks = (int64_t)num_seqs * d.num_kv_heads * pp.tiles;
+  if (blocks > INT32_MAX) return fail(CTX_ERR_INVALID_ARG, "prefill grid too large");
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  const uint16_t* qp = static_cast<const uint16_t*>(q);
+  const uint16_t* kp = static_cast<const uint16_t*>(k_cache);
+  const uint16_t* vp = static_cast<const uint16_t*>(v_cache);
+  if (d.out_dtype == CTX_DTYPE_F32)
+    hipLaunchKernelGGL(prefill_kernel<float>, dim3((unsigned)blocks), dim3(64 * kPrefillWaves), 0, s, qp,
+                       kp, vp, seq_offsets, seq_lens, q_starts, q_lens, pp, static_cast<float*>(out));
+  else
+    hipLaunchKernelGGL(prefill_kernel<uint16_t>, dim3((unsigned)blocks), dim3(64 * kPrefillWaves), 0, s,
+                       qp, kp, vp, seq_offsets, seq_lens, q_starts, q_lens, pp, static_cast<uint16_t*>(out));
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return hip_fail(e, "kernel launch");
+  return CTX_OK;
 }
 
 int ctx_decode_attn_destroy(ctx_decode_attn* h) {

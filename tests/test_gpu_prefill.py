@@ -1,0 +1,152 @@
+"""Causal prefill of the newest tokens (the appended reference observation)
+against the cache, through ctx_prefill_attn_run, against the CPU oracle."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2609_36608_amd import binding as bd
+from paper_2609_36608_amd import workloads as wl
+from paper_2609_36608_amd.binding import CtxError, DecodeAttention
+
+from _gpu_util import assert_parity, dev, up_bf16, up_i32
+
+pytestmark = pytest.mark.gpu
+
+bf = wl.f32_to_bf16_bits
+
+
+def rand_bits(rng, shape):
+    return bf(rng.standard_normal(shape).astype(np.float32))
+
+
+def prefill_case(seed, hq, hkv, batch, hist, new, peaky=False):
+    """History lengths U{hist}, new tokens U{new}; regions shuffled with NaN
+    gaps; query rows placed in shuffled order with unused rows between."""
+    rng = np.random.default_rng(seed)
+    nq = rng.integers(new[0], new[1] + 1, size=batch).astype(np.int32)
+    lens = (rng.integers(hist[0], hist[1] + 1, size=batch) + nq).astype(np.int32)
+    lay = wl.make_layout(lens, 1, gap_max=5, shuffle=True, rng=rng)
+    w = wl.Workload(f"pf{seed}", 150 + seed % 40, 1, batch, hq, hkv, 1, "uniform", 1, 2,
+                    peaky_frac=0.05 if peaky else 0.0)
+    k, v = wl.layer_kv_bits(w, lay, 0, fill=wl.BF16_NAN)
+    order = rng.permutation(batch)
+    q_starts = np.zeros(batch, np.int32)
+    row = 0
+    for b in order:
+        row += int(rng.integers(0, 3))
+        q_starts[b] = row
+        row += int(nq[b])
+    total_q = row + 2
+    q = rand_bits(rng, (total_q, hq, 128))
+    return w, lay, lens, nq, q_starts, q, k, v
+
+
+def run_prefill(w, lay, lens, nq, q_starts, q, k, v, out_dtype=torch.float32):
+    total_q = q.shape[0]
+    with DecodeAttention(w.num_q_heads, w.num_kv_heads, len(lens), int(lens.max()), out_dtype=out_dtype) as attn:
+        out = torch.full((total_q, w.num_q_heads, 128), -555.0, dtype=out_dtype, device=dev())
+        attn.prefill(up_bf16(q), up_bf16(k), up_bf16(v), up_i32(lay.offsets), up_i32(lens), up_i32(q_starts),
+                     up_i32(nq), int(nq.max()), w.scale, out)
+        torch.cuda.synchronize()
+    return out.float().cpu().numpy()
+
+
+@pytest.mark.parametrize("hq,hkv", [(32, 8), (16, 8), (16, 16), (16, 1), (64, 8)])
+def test_prefill_parity(hq, hkv):
+    w, lay, lens, nq, qs, q, k, v = prefill_case(hq * 3 + hkv, hq, hkv, batch=7, hist=(0, 500), new=(1, 140))
+    nq[0], nq[1] = 1, 128 // (hq // hkv) + 1  # decode-like and one past a workgroup tile
+    lens[1] = max(lens[1], nq[1])
+    ref = oracle.prefill_attn(q, k, v, lay.offsets, lens, qs, nq, w.scale)
+    got = run_prefill(w, lay, lens, nq, qs, q, k, v)
+    rows = np.zeros(q.shape[0], bool)
+    for b in range(len(lens)):
+        rows[qs[b]:qs[b] + nq[b]] = True
+    assert_parity(got[rows], ref[rows], f"prefill {hq}/{hkv}")
+    assert (got[~rows] == -555.0).all(), "wrote a row of no sequence"
+
+
+def test_prefill_fresh_prompt_and_peaky_keys():
+    """No history (the whole sequence is new: query 0 sees only itself) and
+    peaky keys, as in the act-first burst."""
+    w, lay, lens, nq, qs, q, k, v = prefill_case(7, 32, 8, batch=5, hist=(0, 0), new=(1, 300), peaky=True)
+    ref = oracle.prefill_attn(q, k, v, lay.offsets, lens, qs, nq, w.scale)
+    got = run_prefill(w, lay, lens, nq, qs, q, k, v)
+    rows = np.concatenate([np.arange(qs[b], qs[b] + nq[b]) for b in range(5)])
+    assert_parity(got[rows], ref[rows], "fresh prompt")
+
+
+def test_prefill_last_row_equals_decode():
+    """The last new token's prefill row is a decode over the whole sequence."""
+    w, lay, lens, nq, qs, q, k, v = prefill_case(11, 32, 8, batch=6, hist=(50, 900), new=(1, 60))
+    got = run_prefill(w, lay, lens, nq, qs, q, k, v)
+    last = qs + nq - 1
+    with DecodeAttention(32, 8, 6, int(lens.max())) as attn:
+        out = torch.empty((6, 32, 128), dtype=torch.float32, device=dev())
+        attn.run(up_bf16(q[last]), up_bf16(k), up_bf16(v), up_i32(lay.offsets), up_i32(lens), w.scale, out)
+        torch.cuda.synchronize()
+    np.testing.assert_allclose(got[last], out.cpu().numpy(), rtol=0, atol=2e-5)
+
+
+def test_prefill_full_size_act_first_burst_sampled():
+    """Act-first burst shape: 256 sequences, history U{4096..12288} plus an
+    appended reference observation of U{128..512} tokens, prefilled in one
+    call.  Sampled query rows are recomputed by the oracle as decodes of
+    their prefixes."""
+    w = wl.WORKLOADS["act_first_burst"]
+    rng = np.random.default_rng(17)
+    lens = wl.draw_lengths(w)                       # history + reference observation
+    nq = wl.rng_for(wl.DEFAULT_SEED, w.index, 0, 5).integers(w.extra_lo, w.extra_hi + 1, size=w.batch).astype(np.int32)
+    lay = wl.make_layout(lens, 1)
+    k = torch.empty((lay.num_rows, 8, 128), dtype=torch.bfloat16, device=dev())
+    v = torch.empty_like(k)
+    wl.fill_normal_bf16_device(k, 42, w.index, 0, 11)
+    wl.fill_normal_bf16_device(v, 42, w.index, 0, 12)
+    q_starts = np.concatenate([[0], np.cumsum(nq)[:-1]]).astype(np.int32)
+    total_q = int(nq.sum())
+    q = rand_bits(rng, (total_q, 32, 128))
+    out = torch.empty((total_q, 32, 128), dtype=torch.float32, device=dev())
+    with DecodeAttention(32, 8, w.batch, int(lens.max())) as attn:
+        attn.prefill(up_bf16(q), k, v, up_i32(lay.offsets), up_i32(lens), up_i32(q_starts), up_i32(nq),
+                     int(nq.max()), w.scale, out)
+        torch.cuda.synchronize()
+    seqs = [int(np.argmax(lens)), int(np.argmin(lens)), 3, 100]
+    hk, hv, sub_offs, sub_lens, rows = [], [], [], [], []
+    base = 0
+    for b in seqs:
+        o, L = int(lay.offsets[b]), int(lens[b])
+        hk.append(k[o:o + L].view(torch.int16).cpu().numpy().view(np.uint16))
+        hv.append(v[o:o + L].view(torch.int16).cpu().numpy().view(np.uint16))
+        for i in sorted(set([0, int(nq[b]) - 1] + list(rng.integers(0, nq[b], size=6)))):
+            rows.append(q_starts[b] + i)
+            sub_offs.append(base)
+            sub_lens.append(L - int(nq[b]) + i + 1)
+        base += L
+    hk, hv = np.concatenate(hk), np.concatenate(hv)
+    ref = oracle.decode_attn(q[rows], hk, hv, np.array(sub_offs), np.array(sub_lens), w.scale)
+    assert_parity(out.cpu().numpy()[rows], ref, f"prefill act-first burst, {len(rows)} sampled rows")
+    assert np.isfinite(out.cpu().numpy()).all()
+
+
+def test_prefill_abi():
+    lib = bd.load_library()
+    with DecodeAttention(24, 8, 2, 32) as attn:  # group 3 does not divide 16
+        z = torch.zeros((2, 24, 128), dtype=torch.bfloat16, device=dev())
+        kv = torch.zeros((8, 8, 128), dtype=torch.bfloat16, device=dev())
+        i = torch.zeros(2, dtype=torch.int32, device=dev())
+        o = torch.zeros((2, 24, 128), dtype=torch.float32, device=dev())
+        with pytest.raises(CtxError):
+            attn.prefill(z, kv, kv, i, i, i, i, 1, 0.1, o)
+    with DecodeAttention(32, 8, 2, 32) as attn:
+        h = attn.handle
+        z = torch.zeros((2, 32, 128), dtype=torch.bfloat16, device=dev())
+        kv = torch.zeros((8, 8, 128), dtype=torch.bfloat16, device=dev())
+        i = torch.zeros(2, dtype=torch.int32, device=dev())
+        o = torch.zeros((2, 32, 128), dtype=torch.float32, device=dev())
+        P = lambda t, off=0: t.data_ptr() + off  # noqa: E731
+        assert lib.ctx_prefill_attn_run(h, P(z), P(kv), P(kv), P(i), P(i), P(i), P(i), 2, 0, 0.1, P(o), None) == bd.CTX_OK
+        assert lib.ctx_prefill_attn_run(h, P(z), P(kv), P(kv), P(i), P(i), P(i), P(i), 3, 1, 0.1, P(o), None) == bd.CTX_ERR_CAPACITY
+        assert lib.ctx_prefill_attn_run(h, P(z, 2), P(kv), P(kv), P(i), P(i), P(i), P(i), 2, 1, 0.1, P(o), None) == bd.CTX_ERR_ALIGNMENT
+        assert lib.ctx_prefill_attn_run(h, P(z), P(kv), P(kv), P(i), P(i), P(i), None, 2, 1, 0.1, P(o), None) == bd.CTX_ERR_INVALID_ARG
+        assert lib.ctx_prefill_attn_run(h, P(z), P(kv), P(kv), P(i), P(i), P(i), P(i), 2, -1, 0.1, P(o), None) == bd.CTX_ERR_INVALID_ARG
+        torch.cuda.synchronize()
