@@ -106,6 +106,171 @@ def cpu_baseline(w: wl.Workload, layout: wl.Layout, target_s: float, threads: in
     }
 
 
+PREFILL_METRIC = "causal prefill attention TFLOP/s (fraction of 2.5 PFLOP/s bf16 MFMA peak), 1 MI355X"
+MFMA_BF16_PEAK_TFLOPS = 2500.0
+
+
+def prefill_flops(lens: np.ndarray, nq: np.ndarray, w: wl.Workload) -> int:
+    """Algorithmic flops of one prefill call: query i of sequence b attends to
+    L_b - nq_b + i + 1 positions, each costing 2*D for q.k and 2*D for p.v per head."""
+    L = lens.astype(np.int64)
+    n = nq.astype(np.int64)
+    positions = n * (L - n) + n * (n + 1) // 2
+    return int(positions.sum()) * 4 * w.head_dim * w.num_q_heads
+
+
+def prefill_cpu_baseline(w, lens, nq, target_s, threads) -> dict:
+    """The CPU oracle on the reference-observation prefill of a few whole sequences."""
+    import oracle
+
+    picks = [0, 1, 2, 3]
+    sl = lens[picks].astype(np.int32)
+    sq = nq[picks].astype(np.int32)
+    offs = np.concatenate([[0], np.cumsum(sl)[:-1]]).astype(np.int32)
+    qs = np.concatenate([[0], np.cumsum(sq)[:-1]]).astype(np.int32)
+    k = np.empty((int(sl.sum()), w.num_kv_heads, w.head_dim), np.uint16)
+    v = np.empty_like(k)
+    for i, b in enumerate(picks):
+        kb, vb = wl.sequence_kv_bits(w, 0, b, int(sl[i]))
+        k[offs[i]:offs[i] + sl[i]] = kb
+        v[offs[i]:offs[i] + sl[i]] = vb
+    rng = np.random.default_rng(7)
+    q = wl.normal_bf16(rng, (int(sq.sum()), w.num_q_heads, w.head_dim))
+    flops = prefill_flops(sl, sq, w)
+    reps, t0 = 0, time.perf_counter()
+    while True:
+        oracle.prefill_attn(q, k, v, offs, sl, qs, sq, w.scale, threads=threads)
+        reps += 1
+        el = time.perf_counter() - t0
+        if el >= target_s or el / reps * (reps + 1) > 3 * target_s:
+            break
+    return {
+        "value": round(flops * reps / el / 1e12, 6),
+        "unit": "TFLOP/s",
+        "cores": threads,
+        "kind": "oracle",
+        "sample": (f"layer 0, sequences {picks} of {w.batch} ({int(sq.sum())} new tokens over "
+                   f"{int(sl.sum())} cached), all {w.num_q_heads} heads, run {reps}x in {el:.1f} s; "
+                   f"float64 C oracle, OpenMP over (query, head)"),
+    }
+
+
+def bench_prefill(args) -> int:
+    """Per layer one ctx_prefill_attn_run: every sequence's appended reference
+    observation (its newest U{128..512} tokens) attends causally over its whole
+    cached history.  A step = all layers."""
+    import torch
+
+    from paper_2609_36608_amd.binding import DecodeAttention
+
+    if not torch.cuda.is_available():
+        print("bench.py: no GPU visible", file=sys.stderr)
+        return 1
+    dev = torch.device("cuda", 0)
+    torch.cuda.set_device(dev)
+    w = wl.WORKLOADS[args.workload]
+    if w.extra_hi <= 0:
+        print(f"bench.py: --prefill needs a workload with an appended observation (act_first_burst)",
+              file=sys.stderr)
+        return 2
+    lens = wl.draw_lengths(w)
+    nq = wl.draw_extra(w)
+    layout = wl.make_layout(lens, 1)
+    B = w.batch
+    layer_bytes = layout.num_rows * w.num_kv_heads * w.head_dim * 2 * 2
+    n_buf = max(1, min(w.layers, HBM_BUDGET_BYTES // layer_bytes))
+    t_setup = time.perf_counter()
+    ks, vs = [], []
+    for i in range(n_buf):
+        k = torch.empty((layout.num_rows, w.num_kv_heads, w.head_dim), dtype=torch.bfloat16, device=dev)
+        v = torch.empty_like(k)
+        wl.fill_normal_bf16_device(k, wl.DEFAULT_SEED, w.index, i, 1)
+        wl.fill_normal_bf16_device(v, wl.DEFAULT_SEED, w.index, i, 2)
+        ks.append(k)
+        vs.append(v)
+    total_q = int(nq.sum())
+    q_starts = np.concatenate([[0], np.cumsum(nq)[:-1]]).astype(np.int32)
+    q = torch.empty((total_q, w.num_q_heads, w.head_dim), dtype=torch.bfloat16, device=dev)
+    wl.fill_normal_bf16_device(q, wl.DEFAULT_SEED, w.index, 0, 0)
+    out = torch.empty((total_q, w.num_q_heads, w.head_dim), dtype=torch.float32, device=dev)
+    t_offs = torch.from_numpy(layout.offsets).to(dev)
+    t_lens = torch.from_numpy(lens).to(dev)
+    t_qs = torch.from_numpy(q_starts).to(dev)
+    t_nq = torch.from_numpy(nq).to(dev)
+    torch.cuda.synchronize()
+    setup_s = time.perf_counter() - t_setup
+    attn = DecodeAttention(w.num_q_heads, w.num_kv_heads, B, int(lens.max()))
+    stream = torch.cuda.current_stream()
+    max_q = int(nq.max())
+
+    def step() -> None:
+        for layer in range(w.layers):
+            attn.prefill(q, ks[layer % n_buf], vs[layer % n_buf], t_offs, t_lens, t_qs, t_nq, max_q,
+                         w.scale, out, stream=stream)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    start = torch.cuda.Event(enable_timing=True)
+    stop = torch.cuda.Event(enable_timing=True)
+    start.record(stream)
+    for _ in range(args.steps):
+        step()
+    stop.record(stream)
+    stop.synchronize()
+    torch.cuda.synchronize()
+    elapsed_s = start.elapsed_time(stop) / 1e3
+    calls = args.steps * w.layers
+    flops = prefill_flops(lens, nq, w)
+    tflops = flops * calls / elapsed_s / 1e12
+    kv_bytes = int(lens.astype(np.int64).sum()) * w.num_kv_heads * w.head_dim * 4
+    result = {
+        "metric": PREFILL_METRIC,
+        "value": round(tflops, 2),
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(elapsed_s * 1e3 / args.steps, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {
+            "workload": (f"reference-observation prefill of {w.name}: {w.layers} layers, batch {B}, "
+                         f"{w.num_q_heads}/{w.num_kv_heads} heads, history U{{{w.length_lo}..{w.length_hi}}} "
+                         f"+ U{{{w.extra_lo}..{w.extra_hi}}} new tokens attending causally"),
+            "name": w.name,
+            "new_tokens": total_q,
+            "cached_tokens": int(lens.sum()),
+            "distinct_layer_buffers": n_buf,
+            "seed": wl.DEFAULT_SEED,
+            "parallelism": "none (1 GPU)",
+        },
+        "tokens_per_s": round(total_q * w.layers * args.steps / elapsed_s / w.layers, 1),
+        "roofline": {
+            "bound": "mfma",
+            "achieved": round(flops / (elapsed_s / calls) / 1e12, 2),
+            "peak": MFMA_BF16_PEAK_TFLOPS,
+            "unit": "TFLOP/s",
+            "frac": round(flops / (elapsed_s / calls) / 1e12 / MFMA_BF16_PEAK_TFLOPS, 4),
+            "traffic": None,
+            "kernel": "prefill_kernel (one ctx_prefill_attn_run call per layer)",
+            "flops_per_launch": flops,
+            "kv_bytes_per_launch": kv_bytes,
+            "avg_launch_us": round(elapsed_s / calls * 1e6, 3),
+        },
+        "setup_s": round(setup_s, 1),
+    }
+    if not args.no_cpu_baseline:
+        threads = len(os.sched_getaffinity(0))
+        result["cpu_baseline"] = prefill_cpu_baseline(w, lens, nq, args.cpu_seconds, threads)
+    print(json.dumps(result), flush=True)
+    attn.close()
+    return 0
+
+
 def main() -> int:
     ap = argparse.ArgumentParser(description=__doc__)
     ap.add_argument("--gpus", type=int, default=1)
@@ -115,6 +280,9 @@ def main() -> int:
     ap.add_argument("--graph", action="store_true", help="replay the timed steps from one HIP graph")
     ap.add_argument("--paged", type=int, default=0, metavar="P",
                     help="use P-token pages (shuffled block tables) and append each step's token")
+    ap.add_argument("--prefill", action="store_true",
+                    help="time the causal prefill of the appended reference observation instead "
+                         "(act_first_burst)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--calibrate-copy-gib", type=float, default=0.0,
@@ -129,6 +297,9 @@ def main() -> int:
     if args.steps < 1 or args.warmup < 0:
         print("bench.py: --steps must be >= 1 and --warmup >= 0", file=sys.stderr)
         return 2
+
+    if args.prefill:
+        return bench_prefill(args)
 
     import torch
 

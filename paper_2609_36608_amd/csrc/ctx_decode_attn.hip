@@ -210,6 +210,14 @@ __device__ __forceinline__ u32x4 buf_load16(__amdgpu_buffer_rsrc_t r, int voff, 
   return __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, kLoadAux));
 }
 
+// Cached variant for data that several workgroups re-read (prefill tiles).
+#ifndef CTX_PREFILL_AUX
+#define CTX_PREFILL_AUX 0
+#endif
+__device__ __forceinline__ u32x4 buf_load16_shared(__amdgpu_buffer_rsrc_t r, int voff, int soff) {
+  return __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, CTX_PREFILL_AUX));
+}
+
 // Softmax state of one lane: query head n of the group (lanes with n >= g
 // carry unused columns), for the 4 tokens 4c..4c+3 of each block.
 struct Softmax {
@@ -592,24 +600,61 @@ __global__ __launch_bounds__(64 * kMergeWaves) void decode_merge_kernel(
 // holds their K/V rows.  Query column n of a 16-column MFMA tile is query
 // position n / g, head n % g of one KV group (g divides 16), so every column
 // carries work.  A workgroup of kPrefillWaves waves covers kPrefillCols
-// columns of one (sequence, KV head); the waves share each 16-token K/V block
-// through a double-buffered LDS tile and stream the blocks up to the
-// workgroup's last query position.  The per-block math is the decode
-// kernel's: V transposed by a selector MFMA once per block, then for each of
-// the wave's column tiles S^T = K Q^T, the causal mask, the lazy online
-// softmax and O^T += V^T (P_hi + P_lo)^T.
+// columns of one (sequence, KV head) and streams 32-token K/V blocks, up to
+// its last query position, through a double-buffered LDS tile that all its
+// waves share.  Per 16 tokens and 16 columns a wave computes
+//   S^T = K Q^T                 (4 MFMA 16x16x32, K rows straight from LDS)
+//   causal mask, lazy online softmax, P = P_hi + P_lo (two bf16 terms)
+//   O^T += V^T [P_hi | P_lo]^T  (8 MFMA 16x16x32: the hi and lo terms are the
+//                                two halves of the K dimension, V^T repeated)
+// where the V^T operand comes from the row-major LDS tile through the LDS
+// transpose read, whose 4 values per lane are tokens 4c..4c+3 of one
+// dimension -- the rows the S^T tile gives each lane.
 
 constexpr int kPrefillWaves = 4;
-constexpr int kPrefillTiles = 2;  // 16-column tiles per wave
+#ifndef CTX_PREFILL_TILES
+#define CTX_PREFILL_TILES 3
+#endif
+constexpr int kPrefillTiles = CTX_PREFILL_TILES;  // 16-column tiles per wave
 constexpr int kPrefillCols = kPrefillWaves * kPrefillTiles * 16;
+constexpr int kPrefillBlock = 32;  // tokens per LDS stage
+#ifndef CTX_PREFILL_XCD
+#define CTX_PREFILL_XCD 1
+#endif
 
 struct PrefillPlan {
   int32_t hq;
   int32_t hkv;
   int32_t group;
   int32_t tiles;  // workgroups per (sequence, KV head)
+  int32_t units;  // sequences x KV heads
   float scale_log2;
 };
+
+typedef short s16x8 __attribute__((ext_vector_type(8)));
+
+// LDS tile of K or V: token row t holds its 16 chunks of 8 dimensions with
+// chunk ch at slot ch ^ prefill_swizzle(t): conflict-free for the staging
+// writes, the K operand reads (16 tokens x one chunk) and the transpose reads
+// (4 tokens x 4 dimensions per 16 lanes).
+__device__ __forceinline__ int prefill_swizzle(int t) { return ((t & 7) << 1) | ((t >> 3) & 1); }
+
+// LDS transpose read: in each 16-lane group, lane l receives element l % 4 of
+// the 8-byte rows addressed by lanes l / 4, 4 + l / 4, 8 + l / 4, 12 + l / 4.
+__device__ __forceinline__ s16x4 lds_read_tr16(const uint16_t* p) {
+  typedef s16x4 __attribute__((address_space(3))) * lds_s16x4;
+  return __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4)(p));
+}
+
+// Split p into bf16 hi (round to nearest even) and the bf16 of the exact
+// remainder lo, for a pair of values: hi and lo are packed as (a, b).
+__device__ __forceinline__ void split_bf16x2(float a, float b, uint32_t* hi, uint32_t* lo) {
+  const uint32_t h = pack_bf16x2(a, b);
+  const float ha = __uint_as_float(h << 16);
+  const float hb = __uint_as_float(h & 0xffff0000u);
+  *hi = h;
+  *lo = pack_bf16x2(a - ha, b - hb);
+}
 
 template <typename OutT>
 __global__ __launch_bounds__(64 * kPrefillWaves) void prefill_kernel(
@@ -619,27 +664,42 @@ __global__ __launch_bounds__(64 * kPrefillWaves) void prefill_kernel(
     OutT* __restrict__ out) {
   const int tid = threadIdx.x;
   const int lane = tid & 63;
-  const int wave = tid >> 6;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int n = lane & 15;
   const int c = lane >> 4;
   const int g = pp.group;
+#if CTX_PREFILL_XCD
+  // consecutive workgroups go to different XCDs; keep every tile of a unit on
+  // one XCD so that its L2 serves the tiles' re-reads of the unit's K/V
+  const int slot = blockIdx.x / kXcds;
+  const int tile = slot % pp.tiles;
+  const int unit = (slot / pp.tiles) * kXcds + (int)(blockIdx.x % kXcds);
+  if (unit >= pp.units) return;
+#else
   const int tile = blockIdx.x % pp.tiles;
   const int unit = blockIdx.x / pp.tiles;
+#endif
   const int kv = unit % pp.hkv;
   const int b = unit / pp.hkv;
   const int nq = q_lens[b];
   const int first_q = tile * (kPrefillCols / g);
   if (first_q >= nq) return;  // the whole workgroup: nothing to do
   const int seq_len = lens[b];
+  const int hist = seq_len - nq;  // position of query 0
   const int last_q = (first_q + kPrefillCols / g < nq ? first_q + kPrefillCols / g : nq) - 1;
-  const int kv_end = seq_len - nq + last_q + 1;  // tokens any query of the workgroup attends to
+  const int kv_end = hist + last_q + 1;  // tokens any query of the workgroup attends to
   const size_t row_elems = (size_t)pp.hkv * kHeadDim;
   const int row_bytes = (int)(row_elems * 2);
   const uint16_t* kseq = kc + (size_t)offs[b] * row_elems + (size_t)kv * kHeadDim;
   const uint16_t* vseq = vc + (size_t)offs[b] * row_elems + (size_t)kv * kHeadDim;
 
-  __shared__ __attribute__((aligned(16))) uint16_t lds_k[2][kBlock * kHeadDim];
-  __shared__ __attribute__((aligned(16))) uint16_t lds_v[2][kBlock * kHeadDim];
+  __shared__ __attribute__((aligned(16))) uint16_t lds_k[2][kPrefillBlock * kHeadDim];
+  __shared__ __attribute__((aligned(16))) uint16_t lds_v[2][kPrefillBlock * kHeadDim];
+
+  // logits in log2 units are s * cs with cs >= 0: a negative scale flips the
+  // sign of q instead (exact in bf16), so that max(s) * cs = max(s * cs)
+  const float cs = fabsf(pp.scale_log2);
+  const uint32_t qflip = pp.scale_log2 < 0.f ? 0x80008000u : 0u;
 
   // this lane's query column in each tile: query index qi, head kv * g + hh,
   // attending to positions 0 .. last_pos (columns past the last query attend
@@ -652,22 +712,24 @@ __global__ __launch_bounds__(64 * kPrefillWaves) void prefill_kernel(
     qi[ct] = col / g;
     hh[ct] = col - qi[ct] * g;
     const bool valid = qi[ct] < nq;
-    last_pos[ct] = valid ? seq_len - nq + qi[ct] : kv_end - 1;
+    last_pos[ct] = valid ? hist + qi[ct] : kv_end - 1;
     if (valid) {
       const uint16_t* qrow =
           q + ((size_t)(q_starts[b] + qi[ct]) * pp.hq + (size_t)kv * g + hh[ct]) * kHeadDim + 8 * c;
 #pragma unroll
-      for (int kk = 0; kk < 4; ++kk) qb[ct][kk] = as_bf16x8(load16(qrow + 32 * kk));
+      for (int kk = 0; kk < 4; ++kk) qb[ct][kk] = as_bf16x8(load16(qrow + 32 * kk) ^ qflip);
     } else {
 #pragma unroll
       for (int kk = 0; kk < 4; ++kk) qb[ct][kk] = as_bf16x8(u32x4{0u, 0u, 0u, 0u});
     }
   }
-  bf16x8 sel[2];
-#pragma unroll
-  for (int h = 0; h < 2; ++h)
-#pragma unroll
-    for (int j = 0; j < 8; ++j) sel[h][j] = (8 * c + j == 16 * h + n) ? (__bf16)1.0f : (__bf16)0.0f;
+  // the wave's query positions: tokens at or below mask_from are seen by every
+  // column; tokens from wave_end on by none (a wave past the last query idles)
+  const int wave_q0 = (tile * kPrefillCols + wave * kPrefillTiles * 16) / g;
+  const int wave_q1 = (tile * kPrefillCols + (wave + 1) * kPrefillTiles * 16 - 1) / g;
+  const bool wave_active = wave_q0 < nq;
+  const int mask_from = hist + wave_q0;
+  const int wave_end = hist + (wave_q1 < last_q ? wave_q1 : last_q) + 1;
 
   Softmax st[kPrefillTiles];
   f32x4 o[kPrefillTiles][8];
@@ -678,88 +740,138 @@ __global__ __launch_bounds__(64 * kPrefillWaves) void prefill_kernel(
     for (int nb = 0; nb < 8; ++nb) o[ct][nb] = f32x4{0.f, 0.f, 0.f, 0.f};
   }
 
-  // cooperative block loads: thread tid fetches 16 bytes (chunk tid % 16) of
-  // token tid / 16 of K and of V; past kv_end the buffer bound returns zeros
+  // cooperative block loads: thread tid fetches chunk tid % 16 of tokens
+  // tid / 16 and 16 + tid / 16 of K and of V; past kv_end the buffer bound
+  // returns zeros
   const int ld_tok = tid >> 4;
-  const int ld_slot = ld_tok * kHeadDim + (((tid & 15) ^ ld_tok) << 3);
+  const int ld_slot = ld_tok * kHeadDim + (((tid & 15) ^ prefill_swizzle(ld_tok)) << 3);
   const int voff = ld_tok * row_bytes + (tid & 15) * 16;
-  u32x4 pk, pv;
+  const int voff_hi = voff + 16 * row_bytes;
+  u32x4 pk0, pk1, pv0, pv1;
   {
-    const uint32_t bytes = (uint32_t)((kv_end < kBlock ? kv_end : kBlock) * row_bytes);
-    pk = buf_load16(make_rsrc(kseq, bytes), voff, 0);
-    pv = buf_load16(make_rsrc(vseq, bytes), voff, 0);
-    *reinterpret_cast<u32x4*>(&lds_k[0][ld_slot]) = pk;
-    *reinterpret_cast<u32x4*>(&lds_v[0][ld_slot]) = pv;
+    const uint32_t bytes = (uint32_t)((kv_end < kPrefillBlock ? kv_end : kPrefillBlock) * row_bytes);
+    const __amdgpu_buffer_rsrc_t rk = make_rsrc(kseq, bytes);
+    const __amdgpu_buffer_rsrc_t rv = make_rsrc(vseq, bytes);
+    pk0 = buf_load16_shared(rk, voff, 0);
+    pk1 = buf_load16_shared(rk, voff_hi, 0);
+    pv0 = buf_load16_shared(rv, voff, 0);
+    pv1 = buf_load16_shared(rv, voff_hi, 0);
+    *reinterpret_cast<u32x4*>(&lds_k[0][ld_slot]) = pk0;
+    *reinterpret_cast<u32x4*>(&lds_k[0][ld_slot + 16 * kHeadDim]) = pk1;
+    *reinterpret_cast<u32x4*>(&lds_v[0][ld_slot]) = pv0;
+    *reinterpret_cast<u32x4*>(&lds_v[0][ld_slot + 16 * kHeadDim]) = pv1;
   }
   __syncthreads();
+
+  // per-lane LDS offsets of the operand reads within a 16-token half block
+  int k_off[4];
+#pragma unroll
+  for (int kk = 0; kk < 4; ++kk) k_off[kk] = n * kHeadDim + (((4 * kk + c) ^ prefill_swizzle(n)) << 3);
+  const int v_tok = 4 * c + (n >> 2);
+  const int v_row = v_tok * kHeadDim + 4 * (n & 1);
+  const int v_swz = prefill_swizzle(v_tok);
+  const int v_ch = (n & 3) >> 1;
+
   int buf = 0;
-  for (int t0 = 0; t0 < kv_end; t0 += kBlock) {
-    const bool more = t0 + kBlock < kv_end;
+  for (int t0 = 0; t0 < kv_end; t0 += kPrefillBlock) {
+    const bool more = t0 + kPrefillBlock < kv_end;
     if (more) {  // next block in flight during this one's math
-      const int rem = kv_end - t0 - kBlock;
-      const uint32_t bytes = (uint32_t)((rem < kBlock ? rem : kBlock) * row_bytes);
-      pk = buf_load16(make_rsrc(kseq + (size_t)(t0 + kBlock) * row_elems, bytes), voff, 0);
-      pv = buf_load16(make_rsrc(vseq + (size_t)(t0 + kBlock) * row_elems, bytes), voff, 0);
+      const int rem = kv_end - t0 - kPrefillBlock;
+      const uint32_t bytes = (uint32_t)((rem < kPrefillBlock ? rem : kPrefillBlock) * row_bytes);
+      const __amdgpu_buffer_rsrc_t rk = make_rsrc(kseq + (size_t)(t0 + kPrefillBlock) * row_elems, bytes);
+      const __amdgpu_buffer_rsrc_t rv = make_rsrc(vseq + (size_t)(t0 + kPrefillBlock) * row_elems, bytes);
+      pk0 = buf_load16_shared(rk, voff, 0);
+      pk1 = buf_load16_shared(rk, voff_hi, 0);
+      pv0 = buf_load16_shared(rv, voff, 0);
+      pv1 = buf_load16_shared(rv, voff_hi, 0);
     }
-    u32x4 kr[4], vr[4];
-#pragma unroll
-    for (int kk = 0; kk < 4; ++kk) {
-      const int slot = n * kHeadDim + (((4 * kk + c) ^ n) << 3);
-      kr[kk] = *reinterpret_cast<const u32x4*>(&lds_k[buf][slot]);
-      vr[kk] = *reinterpret_cast<const u32x4*>(&lds_v[buf][slot]);
-    }
-    // V^T operands: lane (c, n) of nb holds V[token 4c+i][dim 16 nb + n]
-    s16x4 vt[8];
-    const f32x4 zero = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-    for (int kk = 0; kk < 4; ++kk)
+    if (wave_active && t0 < wave_end) {
+      const uint16_t* kt = lds_k[buf];
+      const uint16_t* vt = lds_v[buf];
+      // S^T of tokens t0 + 16 h + 4c + i (i < 4) for every column tile
+      f32x4 sc[kPrefillTiles][2];
 #pragma unroll
       for (int h = 0; h < 2; ++h) {
-        const f32x4 t = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(vr[kk]), sel[h], zero, 0, 0, 0);
-        vt[2 * kk + h] = pack_bf16x4(t[0], t[1], t[2], t[3]);
+        u32x4 kr[4];
+#pragma unroll
+        for (int kk = 0; kk < 4; ++kk)
+          kr[kk] = *reinterpret_cast<const u32x4*>(kt + 16 * h * kHeadDim + k_off[kk]);
+#pragma unroll
+        for (int ct = 0; ct < kPrefillTiles; ++ct) sc[ct][h] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int kk = 0; kk < 4; ++kk)
+#pragma unroll
+          for (int ct = 0; ct < kPrefillTiles; ++ct)
+            sc[ct][h] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(kr[kk]), qb[ct][kk], sc[ct][h], 0, 0, 0);
       }
+      const bool masked = t0 + kPrefillBlock - 1 > mask_from;
+      u32x4 phi[kPrefillTiles], plo[kPrefillTiles];
 #pragma unroll
-    for (int ct = 0; ct < kPrefillTiles; ++ct) {
-      f32x4 s = {0.f, 0.f, 0.f, 0.f};
+      for (int ct = 0; ct < kPrefillTiles; ++ct) {
+        float x[8];
+        float lmax;
+        if (masked) {  // blocks on the causal diagonal (or past kv_end)
 #pragma unroll
-      for (int kk = 0; kk < 4; ++kk)
-        s = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(kr[kk]), qb[ct][kk], s, 0, 0, 0);
-      float x[4];
+          for (int h = 0; h < 2; ++h)
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        x[i] = s[i] * pp.scale_log2;
-        if (t0 + 4 * c + i > last_pos[ct]) x[i] = -INFINITY;  // causal (and past kv_end)
+            for (int i = 0; i < 4; ++i)
+              x[4 * h + i] = (t0 + 16 * h + 4 * c + i > last_pos[ct]) ? -INFINITY : sc[ct][h][i] * cs;
+          lmax = fmaxf(fmaxf(fmaxf(x[0], x[1]), fmaxf(x[2], x[3])), fmaxf(fmaxf(x[4], x[5]), fmaxf(x[6], x[7])));
+        } else {
+          const f32x4 a = sc[ct][0], e = sc[ct][1];
+          lmax = fmaxf(fmaxf(fmaxf(a[0], a[1]), fmaxf(a[2], a[3])), fmaxf(fmaxf(e[0], e[1]), fmaxf(e[2], e[3]))) * cs;
+        }
+        // lazy rescale: only when some logit exceeds the running max by 2^8;
+        // the column max (across the 4 lanes of a column) only then
+        if (__any(lmax > st[ct].m + kLazyRescale)) {
+          float mx = fmaxf(lmax, __shfl_xor(lmax, 16));
+          mx = fmaxf(mx, __shfl_xor(mx, 32));
+          const float m_new = fmaxf(st[ct].m, mx);
+          const float alpha = fast_exp2(st[ct].m - m_new);
+          st[ct].l *= alpha;
+#pragma unroll
+          for (int nb = 0; nb < 8; ++nb) o[ct][nb] *= alpha;
+          st[ct].m = m_new;
+        }
+        float pr[8];
+        if (masked) {
+#pragma unroll
+          for (int i = 0; i < 8; ++i) pr[i] = fast_exp2(x[i] - st[ct].m);
+        } else {
+#pragma unroll
+          for (int h = 0; h < 2; ++h)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) pr[4 * h + i] = fast_exp2(fmaf(sc[ct][h][i], cs, -st[ct].m));
+        }
+        st[ct].l += ((pr[0] + pr[1]) + (pr[2] + pr[3])) + ((pr[4] + pr[5]) + (pr[6] + pr[7]));
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          uint32_t hw, lw;
+          split_bf16x2(pr[2 * j], pr[2 * j + 1], &hw, &lw);
+          phi[ct][j] = hw;
+          plo[ct][j] = lw;
+        }
       }
-      float mx = fmaxf(fmaxf(x[0], x[1]), fmaxf(x[2], x[3]));
-      mx = fmaxf(mx, __shfl_xor(mx, 16));
-      mx = fmaxf(mx, __shfl_xor(mx, 32));
-      if (__any(mx > st[ct].m + kLazyRescale)) {
-        const float m_new = fmaxf(st[ct].m, mx);
-        const float alpha = fast_exp2(st[ct].m - m_new);
-        st[ct].l *= alpha;
-#pragma unroll
-        for (int nb = 0; nb < 8; ++nb) o[ct][nb] *= alpha;
-        st[ct].m = m_new;
-      }
-      float pr[4], hi[4], lo[4];
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        pr[i] = fast_exp2(x[i] - st[ct].m);
-        hi[i] = (float)(__bf16)pr[i];
-        lo[i] = pr[i] - hi[i];
-      }
-      st[ct].l += (pr[0] + pr[1]) + (pr[2] + pr[3]);
-      const s16x4 p_hi = pack_bf16x4(hi[0], hi[1], hi[2], hi[3]);
-      const s16x4 p_lo = pack_bf16x4(lo[0], lo[1], lo[2], lo[3]);
+      // O^T += V^T P^T: the K dimension holds tokens 4c..4c+3 of both halves
 #pragma unroll
       for (int nb = 0; nb < 8; ++nb) {
-        o[ct][nb] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(vt[nb], p_hi, o[ct][nb], 0, 0, 0);
-        o[ct][nb] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(vt[nb], p_lo, o[ct][nb], 0, 0, 0);
+        const int off = v_row + (((2 * nb + v_ch) ^ v_swz) << 3);
+        const s16x4 v0 = lds_read_tr16(vt + off);
+        const s16x4 v1 = lds_read_tr16(vt + 16 * kHeadDim + off);
+        const bf16x8 va = __builtin_bit_cast(bf16x8, __builtin_shufflevector(v0, v1, 0, 1, 2, 3, 4, 5, 6, 7));
+#pragma unroll
+        for (int ct = 0; ct < kPrefillTiles; ++ct)
+          o[ct][nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(va, as_bf16x8(phi[ct]), o[ct][nb], 0, 0, 0);
+#pragma unroll
+        for (int ct = 0; ct < kPrefillTiles; ++ct)
+          o[ct][nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(va, as_bf16x8(plo[ct]), o[ct][nb], 0, 0, 0);
       }
     }
     if (more) {  // the other buffer was released at the previous barrier
-      *reinterpret_cast<u32x4*>(&lds_k[buf ^ 1][ld_slot]) = pk;
-      *reinterpret_cast<u32x4*>(&lds_v[buf ^ 1][ld_slot]) = pv;
+      *reinterpret_cast<u32x4*>(&lds_k[buf ^ 1][ld_slot]) = pk0;
+      *reinterpret_cast<u32x4*>(&lds_k[buf ^ 1][ld_slot + 16 * kHeadDim]) = pk1;
+      *reinterpret_cast<u32x4*>(&lds_v[buf ^ 1][ld_slot]) = pv0;
+      *reinterpret_cast<u32x4*>(&lds_v[buf ^ 1][ld_slot + 16 * kHeadDim]) = pv1;
     }
     __syncthreads();
     buf ^= 1;
@@ -1049,7 +1161,8 @@ int ctx_prefill_attn_run(ctx_decode_attn* h, const void* q, const void* k_cache,
   pp.group = g;
   pp.tiles = (int32_t)(((int64_t)max_q_len * g + kPrefillCols - 1) / kPrefillCols);
   pp.scale_log2 = (float)((double)scale * 1.4426950408889634);
-  const int64_t blocks = (int64_t)num_seqs * d.num_kv_heads * pp.tiles;
+  pp.units = num_seqs * d.num_kv_heads;
+  const int64_t blocks = (CTX_PREFILL_XCD ? round_up(pp.units, kXcds) : (int64_t)pp.units) * pp.tiles;
   if (blocks > INT32_MAX) return fail(CTX_ERR_INVALID_ARG, "prefill grid too large");
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
   const uint16_t* qp = static_cast<const uint16_t*>(q);

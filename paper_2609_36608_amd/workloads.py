@@ -136,9 +136,17 @@ def draw_lengths(w: Workload, seed: int = DEFAULT_SEED) -> np.ndarray:
     else:
         raise ValueError(w.length_kind)
     if w.extra_hi > 0:
-        rng_x = rng_for(seed, w.index, 0, _T_EXTRA)
-        lens = lens + rng_x.integers(w.extra_lo, w.extra_hi + 1, size=w.batch)
+        lens = lens + draw_extra(w, seed)
     return lens.astype(np.int32)
+
+
+def draw_extra(w: Workload, seed: int = DEFAULT_SEED) -> np.ndarray:
+    """Tokens of the appended reference next observation of every sequence
+    (the newest tokens, already counted in draw_lengths); zeros if none."""
+    if w.extra_hi <= 0:
+        return np.zeros(w.batch, np.int32)
+    rng_x = rng_for(seed, w.index, 0, _T_EXTRA)
+    return rng_x.integers(w.extra_lo, w.extra_hi + 1, size=w.batch).astype(np.int32)
 
 
 @dataclass

@@ -96,7 +96,7 @@ def test_prefill_full_size_act_first_burst_sampled():
     w = wl.WORKLOADS["act_first_burst"]
     rng = np.random.default_rng(17)
     lens = wl.draw_lengths(w)                       # history + reference observation
-    nq = wl.rng_for(wl.DEFAULT_SEED, w.index, 0, 5).integers(w.extra_lo, w.extra_hi + 1, size=w.batch).astype(np.int32)
+    nq = wl.draw_extra(w)
     lay = wl.make_layout(lens, 1)
     k = torch.empty((lay.num_rows, 8, 128), dtype=torch.bfloat16, device=dev())
     v = torch.empty_like(k)
