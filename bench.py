@@ -41,10 +41,10 @@ def algorithmic_bytes(lens: np.ndarray, w: wl.Workload, out_bytes: int = 4) -> i
     return kv + b * w.num_q_heads * w.head_dim * (2 + out_bytes) + 8 * b
 
 
-def profiled_traffic(workload: str):
-    """HBM bytes per split-kernel launch from the committed rocprofv3 counter
-    summary, or None if that summary is for another workload or for an older
-    version of the kernel source."""
+def profiled_traffic(workload: str, kernel: str = "decode_split_kernel"):
+    """HBM bytes per launch of `kernel` from the committed rocprofv3 counter
+    summary, or None if that summary is for another workload or kernel or for
+    an older version of the kernel source."""
     import glob
     import hashlib
 
@@ -56,7 +56,8 @@ def profiled_traffic(workload: str):
             if ":" in line and not line.startswith(("|", "#", "`")):
                 k, _, v = line.partition(":")
                 fields[k.strip()] = v.strip()
-        if fields.get("kernel_source_sha256") == digest and fields.get("workload") == workload:
+        if (fields.get("kernel_source_sha256") == digest and fields.get("workload") == workload
+                and fields.get("kernel", "decode_split_kernel") == kernel):
             t = int(fields["traffic_bytes_per_launch"])
             a = int(fields["algorithmic_bytes_per_launch"])
             return {"bytes_per_launch": t, "ratio_to_algorithmic": round(t / a, 4),
@@ -222,6 +223,13 @@ def bench_prefill(args) -> int:
     elapsed_s = start.elapsed_time(stop) / 1e3
     calls = args.steps * w.layers
     flops = prefill_flops(lens, nq, w)
+    if args.calibrate_copy_gib > 0:
+        ncopy = int(args.calibrate_copy_gib * 2**30) // 4
+        src = torch.ones(ncopy, dtype=torch.float32, device=dev)
+        dst = torch.empty_like(src)
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
     tflops = flops * calls / elapsed_s / 1e12
     kv_bytes = int(lens.astype(np.int64).sum()) * w.num_kv_heads * w.head_dim * 4
     result = {
@@ -255,7 +263,7 @@ def bench_prefill(args) -> int:
             "peak": MFMA_BF16_PEAK_TFLOPS,
             "unit": "TFLOP/s",
             "frac": round(flops / (elapsed_s / calls) / 1e12 / MFMA_BF16_PEAK_TFLOPS, 4),
-            "traffic": None,
+            "traffic": profiled_traffic(w.name, "prefill_kernel"),
             "kernel": "prefill_kernel (one ctx_prefill_attn_run call per layer)",
             "flops_per_launch": flops,
             "kv_bytes_per_launch": kv_bytes,

@@ -611,13 +611,20 @@ __global__ __launch_bounds__(64 * kMergeWaves) void decode_merge_kernel(
 // transpose read, whose 4 values per lane are tokens 4c..4c+3 of one
 // dimension -- the rows the S^T tile gives each lane.
 
-constexpr int kPrefillWaves = 4;
+#ifndef CTX_PREFILL_WAVES
+#define CTX_PREFILL_WAVES 4
+#endif
+constexpr int kPrefillWaves = CTX_PREFILL_WAVES;
 #ifndef CTX_PREFILL_TILES
 #define CTX_PREFILL_TILES 3
 #endif
 constexpr int kPrefillTiles = CTX_PREFILL_TILES;  // 16-column tiles per wave
 constexpr int kPrefillCols = kPrefillWaves * kPrefillTiles * 16;
 constexpr int kPrefillBlock = 32;  // tokens per LDS stage
+// 16-byte chunks each thread stages per K (and per V) block
+constexpr int kPrefillLoads = kPrefillBlock * 16 / (64 * kPrefillWaves);
+static_assert(kPrefillLoads >= 1 && kPrefillLoads * 64 * kPrefillWaves == kPrefillBlock * 16,
+              "the workgroup must tile a block's chunks exactly");
 #ifndef CTX_PREFILL_XCD
 #define CTX_PREFILL_XCD 1
 #endif
@@ -646,14 +653,13 @@ __device__ __forceinline__ s16x4 lds_read_tr16(const uint16_t* p) {
   return __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4)(p));
 }
 
-// Split p into bf16 hi (round to nearest even) and the bf16 of the exact
-// remainder lo, for a pair of values: hi and lo are packed as (a, b).
+// Split a pair of non-negative floats into bf16 hi = the value with its low 16
+// bits cleared and bf16 lo = round-to-nearest-even of the exact remainder, so
+// that hi + lo carries 16 significant bits; both packed as (a, b).
 __device__ __forceinline__ void split_bf16x2(float a, float b, uint32_t* hi, uint32_t* lo) {
-  const uint32_t h = pack_bf16x2(a, b);
-  const float ha = __uint_as_float(h << 16);
-  const float hb = __uint_as_float(h & 0xffff0000u);
-  *hi = h;
-  *lo = pack_bf16x2(a - ha, b - hb);
+  const uint32_t ua = __float_as_uint(a), ub = __float_as_uint(b);
+  *hi = __builtin_amdgcn_perm(ub, ua, 0x07060302u);  // high halves of a and b
+  *lo = pack_bf16x2(a - __uint_as_float(ua & 0xffff0000u), b - __uint_as_float(ub & 0xffff0000u));
 }
 
 template <typename OutT>
@@ -741,25 +747,30 @@ __global__ __launch_bounds__(64 * kPrefillWaves) void prefill_kernel(
   }
 
   // cooperative block loads: thread tid fetches chunk tid % 16 of tokens
-  // tid / 16 and 16 + tid / 16 of K and of V; past kv_end the buffer bound
-  // returns zeros
-  const int ld_tok = tid >> 4;
-  const int ld_slot = ld_tok * kHeadDim + (((tid & 15) ^ prefill_swizzle(ld_tok)) << 3);
-  const int voff = ld_tok * row_bytes + (tid & 15) * 16;
-  const int voff_hi = voff + 16 * row_bytes;
-  u32x4 pk0, pk1, pv0, pv1;
+  // tid / 16 + r * (4 * kPrefillWaves), r < kPrefillLoads, of K and of V; past
+  // kv_end the buffer bound returns zeros
+  int ld_slot[kPrefillLoads], voff[kPrefillLoads];
+#pragma unroll
+  for (int r = 0; r < kPrefillLoads; ++r) {
+    const int t = (tid >> 4) + r * 4 * kPrefillWaves;
+    ld_slot[r] = t * kHeadDim + (((tid & 15) ^ prefill_swizzle(t)) << 3);
+    voff[r] = t * row_bytes + (tid & 15) * 16;
+  }
+  u32x4 pk[kPrefillLoads], pv[kPrefillLoads];
   {
     const uint32_t bytes = (uint32_t)((kv_end < kPrefillBlock ? kv_end : kPrefillBlock) * row_bytes);
     const __amdgpu_buffer_rsrc_t rk = make_rsrc(kseq, bytes);
     const __amdgpu_buffer_rsrc_t rv = make_rsrc(vseq, bytes);
-    pk0 = buf_load16_shared(rk, voff, 0);
-    pk1 = buf_load16_shared(rk, voff_hi, 0);
-    pv0 = buf_load16_shared(rv, voff, 0);
-    pv1 = buf_load16_shared(rv, voff_hi, 0);
-    *reinterpret_cast<u32x4*>(&lds_k[0][ld_slot]) = pk0;
-    *reinterpret_cast<u32x4*>(&lds_k[0][ld_slot + 16 * kHeadDim]) = pk1;
-    *reinterpret_cast<u32x4*>(&lds_v[0][ld_slot]) = pv0;
-    *reinterpret_cast<u32x4*>(&lds_v[0][ld_slot + 16 * kHeadDim]) = pv1;
+#pragma unroll
+    for (int r = 0; r < kPrefillLoads; ++r) {
+      pk[r] = buf_load16_shared(rk, voff[r], 0);
+      pv[r] = buf_load16_shared(rv, voff[r], 0);
+    }
+#pragma unroll
+    for (int r = 0; r < kPrefillLoads; ++r) {
+      *reinterpret_cast<u32x4*>(&lds_k[0][ld_slot[r]]) = pk[r];
+      *reinterpret_cast<u32x4*>(&lds_v[0][ld_slot[r]]) = pv[r];
+    }
   }
   __syncthreads();
 
@@ -780,10 +791,11 @@ __global__ __launch_bounds__(64 * kPrefillWaves) void prefill_kernel(
       const uint32_t bytes = (uint32_t)((rem < kPrefillBlock ? rem : kPrefillBlock) * row_bytes);
       const __amdgpu_buffer_rsrc_t rk = make_rsrc(kseq + (size_t)(t0 + kPrefillBlock) * row_elems, bytes);
       const __amdgpu_buffer_rsrc_t rv = make_rsrc(vseq + (size_t)(t0 + kPrefillBlock) * row_elems, bytes);
-      pk0 = buf_load16_shared(rk, voff, 0);
-      pk1 = buf_load16_shared(rk, voff_hi, 0);
-      pv0 = buf_load16_shared(rv, voff, 0);
-      pv1 = buf_load16_shared(rv, voff_hi, 0);
+#pragma unroll
+      for (int r = 0; r < kPrefillLoads; ++r) {
+        pk[r] = buf_load16_shared(rk, voff[r], 0);
+        pv[r] = buf_load16_shared(rv, voff[r], 0);
+      }
     }
     if (wave_active && t0 < wave_end) {
       const uint16_t* kt = lds_k[buf];
@@ -868,10 +880,11 @@ __global__ __launch_bounds__(64 * kPrefillWaves) void prefill_kernel(
       }
     }
     if (more) {  // the other buffer was released at the previous barrier
-      *reinterpret_cast<u32x4*>(&lds_k[buf ^ 1][ld_slot]) = pk0;
-      *reinterpret_cast<u32x4*>(&lds_k[buf ^ 1][ld_slot + 16 * kHeadDim]) = pk1;
-      *reinterpret_cast<u32x4*>(&lds_v[buf ^ 1][ld_slot]) = pv0;
-      *reinterpret_cast<u32x4*>(&lds_v[buf ^ 1][ld_slot + 16 * kHeadDim]) = pv1;
+#pragma unroll
+      for (int r = 0; r < kPrefillLoads; ++r) {
+        *reinterpret_cast<u32x4*>(&lds_k[buf ^ 1][ld_slot[r]]) = pk[r];
+        *reinterpret_cast<u32x4*>(&lds_v[buf ^ 1][ld_slot[r]]) = pv[r];
+      }
     }
     __syncthreads();
     buf ^= 1;
