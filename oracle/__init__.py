@@ -1,4 +1,5 @@
-"""CPU oracle for decode-step GQA attention (test infrastructure only).
+"""CPU oracles for decode-step GQA attention, causal prefill and the OPD token
+loss (test infrastructure only).
 
 Only the tests, the smoke check and the benchmark's CPU-baseline leg may use
 this package.  It wraps `liboracle_attn.so` (plain C, double precision) with
@@ -35,6 +36,14 @@ def _load():
         lib.oracle_decode_attn_paged_pairs.restype = ctypes.c_int
         lib.oracle_prefill_attn.argtypes = [p, p, p, p, p, p, p, i32, i32, i32, i32, i64, i64, f64, p, i32]
         lib.oracle_prefill_attn.restype = ctypes.c_int
+        lib.oracle_opd_loss.argtypes = [p, i64, i32, p, p, p, p, p, i32, i32, f64, f64, f64, f64,
+                                        p, p, p, p, p, i32]
+        lib.oracle_opd_loss.restype = ctypes.c_int
+        lib.oracle_opd_loss_f64.argtypes = [p, i32, p, p, p, p, p, i32, i32, f64, f64, f64, f64,
+                                            p, p, p, p, p, i32]
+        lib.oracle_opd_loss_f64.restype = ctypes.c_int
+        lib.oracle_opd_grad_rows.argtypes = [p, i64, i32, p, p, p, p, i64, p, i32]
+        lib.oracle_opd_grad_rows.restype = ctypes.c_int
         _lib = lib
     return _lib
 
@@ -141,4 +150,53 @@ def prefill_attn(q, k, v, seq_offsets, seq_lens, q_starts, q_lens, scale, thread
     out = np.zeros((total_q, hq, d), dtype=np.float64)
     _check(_load().oracle_prefill_attn(_ptr(q), _ptr(k), _ptr(v), _ptr(offs), _ptr(lens), _ptr(qs), _ptr(ql),
                                        len(lens), hq, hkv, d, rows, total_q, float(scale), _ptr(out), threads))
+    return out
+
+
+# OPD loss constants of the paper (App. OPD Optimization, tab:training-hyperparameters)
+OPD_CLIP_LOG = 20.0
+OPD_DELTA = 0.2
+OPD_KAPPA = 3.0
+OPD_EPS = 1e-8
+
+
+def _opd_common(tokens, old_lp, tea_lp, mask, seq_starts):
+    return (_i32(tokens), np.ascontiguousarray(old_lp, dtype=np.float32),
+            np.ascontiguousarray(tea_lp, dtype=np.float32), np.ascontiguousarray(mask, dtype=np.uint8),
+            _i32(seq_starts))
+
+
+def opd_loss(logits, tokens, old_lp, tea_lp, mask, seq_starts, clip_log=OPD_CLIP_LOG, delta=OPD_DELTA,
+             kappa=OPD_KAPPA, eps=OPD_EPS, threads: int = 0) -> dict:
+    """OPD surrogate loss over a packed batch.  logits: bf16 bits [N, stride]
+    (the first `vocab` columns used; pass vocab via a [N, V] array) or float64
+    [N, V].  Returns float64 loss and per-token lp, weight, token_loss and
+    dlp (= dL/dlp_j)."""
+    tok, old, tea, m, st = _opd_common(tokens, old_lp, tea_lp, mask, seq_starts)
+    n = len(tok)
+    lp, w, tl, dlp = (np.zeros(n, np.float64) for _ in range(4))
+    loss = np.zeros(1, np.float64)
+    if logits.dtype == np.float64:
+        z = np.ascontiguousarray(logits)
+        rc = _load().oracle_opd_loss_f64(_ptr(z), z.shape[1], _ptr(tok), _ptr(old), _ptr(tea), _ptr(m), _ptr(st),
+                                         len(st) - 1, n, clip_log, delta, kappa, eps, _ptr(lp), _ptr(w),
+                                         _ptr(tl), _ptr(dlp), _ptr(loss), threads)
+    else:
+        z = _u16(logits)
+        rc = _load().oracle_opd_loss(_ptr(z), z.shape[1], z.shape[1], _ptr(tok), _ptr(old), _ptr(tea), _ptr(m),
+                                     _ptr(st), len(st) - 1, n, clip_log, delta, kappa, eps, _ptr(lp), _ptr(w),
+                                     _ptr(tl), _ptr(dlp), _ptr(loss), threads)
+    _check(rc)
+    return {"loss": float(loss[0]), "lp": lp, "weight": w, "token_loss": tl, "dlp": dlp}
+
+
+def opd_grad_rows(logits, tokens, mask, dlp, rows, threads: int = 0) -> np.ndarray:
+    """dL/dlogits for the listed rows, float64 [len(rows), V]; logits bf16 bits [N, V]."""
+    z = _u16(logits)
+    tok, m = _i32(tokens), np.ascontiguousarray(mask, dtype=np.uint8)
+    d = np.ascontiguousarray(dlp, dtype=np.float64)
+    r = np.ascontiguousarray(rows, dtype=np.int64)
+    out = np.zeros((len(r), z.shape[1]), np.float64)
+    _check(_load().oracle_opd_grad_rows(_ptr(z), z.shape[1], z.shape[1], _ptr(tok), _ptr(m), _ptr(d), _ptr(r),
+                                        len(r), _ptr(out), threads))
     return out

@@ -466,3 +466,176 @@ def test_prefill_rejects_bad_lengths():
         oracle.prefill_attn(q, k, k, [0], [3], [0], [4], 0.1)   # more queries than tokens
     with pytest.raises(ValueError):
         oracle.prefill_attn(q, k, k, [0], [8], [2], [3], 0.1)   # query rows past q
+
+
+# ---------------------------------------------------------------- OPD token loss
+# App. OPD Optimization: eq:opd-token-advantage, eq:opd-ratio, eq:opd-dual-clip,
+# eq:opd-surrogate (delta = 0.2, kappa = 3, ratio clip 20, eps = 1e-8).
+
+def _one_hot_rows(n, vocab=4):
+    """Rows whose token 0 has log-probability 0 to far below double rounding."""
+    z = np.full((n, vocab), -100.0)
+    z[:, 0] = 0.0
+    return z
+
+
+# (A, rho, token loss, d loss / d rho * rho) from the cases of eq:opd-dual-clip, by hand
+OPD_REGIMES = [
+    (0.5, 0.5, -0.25, -0.25),        # A > 0, below the band: rho A selected
+    (0.5, 1.1, -0.55, -0.55),        # A > 0, inside the band
+    (0.5, 1.5, -0.6, 0.0),           # A > 0, above the band: clip(rho) A = 1.2 A, flat
+    (-0.5, 0.5, 0.4, 0.0),           # A < 0, below the band: clip(rho) A = 0.8 A, flat
+    (-0.5, 1.1, 0.55, 0.55),         # A < 0, inside the band
+    (-0.5, 2.0, 1.0, 1.0),           # A < 0, above the band, under the dual clip
+    (-0.5, 4.0, 1.5, 0.0),           # A < 0, dual clip kappa |A| = 1.5, flat
+    (0.0, 2.0, 0.0, 0.0),            # A = 0
+]
+
+
+def _regime_batch(cases, per_seq=1):
+    n = len(cases)
+    old = np.array([-np.log(rho) for _, rho, _, _ in cases], np.float32)
+    tea = (old.astype(np.float64) + np.array([a for a, _, _, _ in cases])).astype(np.float32)
+    starts = np.arange(0, n + 1, per_seq, dtype=np.int32)
+    return _one_hot_rows(n), np.zeros(n, np.int32), old, tea, np.ones(n, np.uint8), starts
+
+
+def test_opd_regimes_closed_form():
+    z, tok, old, tea, m, st = _regime_batch(OPD_REGIMES)
+    r = oracle.opd_loss(z, tok, old, tea, m, st)
+    n = len(OPD_REGIMES)
+    np.testing.assert_allclose(r["token_loss"], [c[2] for c in OPD_REGIMES], rtol=0, atol=1e-6)
+    w = 1.0 / (n * (1 + 1e-8))
+    np.testing.assert_allclose(r["weight"], w, rtol=1e-12)
+    np.testing.assert_allclose(r["dlp"], [w * c[3] for c in OPD_REGIMES], rtol=0, atol=1e-7)
+    np.testing.assert_allclose(r["lp"], 0.0, atol=1e-30)
+
+
+def test_opd_ratio_clip_at_20():
+    # lp - old = 25 is clipped to 20 (eq:opd-ratio): rho = e^20, no gradient through rho
+    # lp - old = -25 clips to -20: rho = e^-20, below the band, where the loss
+    # -rho A has a slope in rho, yet no gradient reaches lp through the clip
+    z = _one_hot_rows(3)
+    old = np.array([-25.0, -25.0, 25.0], np.float32)
+    tea = old + np.array([0.5, -0.5, 0.5], np.float32)
+    r = oracle.opd_loss(z, [0, 0, 0], old, tea, [1, 1, 1], [0, 1, 2, 3])
+    np.testing.assert_allclose(r["token_loss"], [-0.6, 1.5, -0.5 * math.exp(-20)], rtol=1e-6, atol=1e-6)
+    assert (r["dlp"] == 0).all()
+    # just inside the clip the ratio carries gradient again: l = -1.2 A flat for A > 0,
+    # but for A < 0 above the band the dual clip is flat too; use A < 0 below kappa
+    z2 = _one_hot_rows(1)
+    old2 = np.array([-np.log(2.0)], np.float32)
+    r2 = oracle.opd_loss(z2, [0], old2, old2 - np.float32(0.5), [1], [0, 1])
+    assert r2["dlp"][0] > 0
+
+
+def test_opd_seq_mean_token_mean():
+    # response 0: one token with loss -0.25; response 1: three tokens 0.4, 0.55, 1.0
+    # seq-mean-token-mean = (-0.25 + 1.95 / 3) / 2 = 0.2 (token mean would be 0.425)
+    cases = [OPD_REGIMES[0], OPD_REGIMES[3], OPD_REGIMES[4], OPD_REGIMES[5]]
+    z, tok, old, tea, m, _ = _regime_batch(cases)
+    r = oracle.opd_loss(z, tok, old, tea, m, [0, 1, 4])
+    assert r["loss"] == pytest.approx(0.2, abs=1e-6)
+    np.testing.assert_allclose(r["weight"], [0.5 / (1 + 1e-8)] + [0.5 / (3 + 1e-8)] * 3, rtol=1e-12)
+
+
+def test_opd_masked_tokens_are_excluded():
+    # inserted tokens stay in the context but carry no loss and no normalisation;
+    # their rows are never read (NaN logits, garbage log-probs)
+    cases = [OPD_REGIMES[0], OPD_REGIMES[3], OPD_REGIMES[4], OPD_REGIMES[5]]
+    z, tok, old, tea, m, _ = _regime_batch(cases)
+    z = np.insert(z, [2, 4], np.nan, axis=0)
+    tok = np.insert(tok, [2, 4], 3)
+    old = np.insert(old, [2, 4], np.float32(7.0))
+    tea = np.insert(tea, [2, 4], np.float32(-9.0))
+    m = np.insert(m, [2, 4], 0)
+    zb = wl.f32_to_bf16_bits(z.astype(np.float32))
+    r = oracle.opd_loss(zb, tok, old, tea, m, [0, 1, 6])
+    assert r["loss"] == pytest.approx(0.2, abs=1e-5)
+    for j in (2, 5):
+        assert r["token_loss"][j] == 0 and r["dlp"][j] == 0 and r["lp"][j] == 0 and r["weight"][j] == 0
+    g = oracle.opd_grad_rows(zb, tok, m, r["dlp"], [2, 5])
+    assert (g == 0).all()
+
+
+def test_opd_fully_masked_response_counts_in_the_batch():
+    # 0 / (0 + eps) = 0 for a response with no supervised token, and |B| grows
+    cases = [OPD_REGIMES[0], OPD_REGIMES[3], OPD_REGIMES[4], OPD_REGIMES[5], OPD_REGIMES[1]]
+    z, tok, old, tea, m, _ = _regime_batch(cases)
+    m[4] = 0
+    r = oracle.opd_loss(z, tok, old, tea, m, [0, 1, 4, 5])
+    assert r["loss"] == pytest.approx(0.2 * 2 / 3, abs=1e-6)
+    r0 = oracle.opd_loss(z, tok, old, tea, m, [0, 1, 4, 4, 5])  # and an empty response
+    assert r0["loss"] == pytest.approx(0.2 * 2 / 4, abs=1e-6)
+
+
+def test_opd_logprob_is_log_softmax():
+    from scipy.special import logsumexp
+
+    rng = np.random.default_rng(3)
+    zb = wl.f32_to_bf16_bits((3 * rng.standard_normal((8, 1000))).astype(np.float32))
+    z = wl.bf16_bits_to_f32(zb).astype(np.float64)
+    tok = rng.integers(0, 1000, 8).astype(np.int32)
+    r = oracle.opd_loss(zb, tok, np.zeros(8, np.float32), np.zeros(8, np.float32), np.ones(8, np.uint8),
+                        [0, 8])
+    np.testing.assert_allclose(r["lp"], z[np.arange(8), tok] - logsumexp(z, axis=1), rtol=0, atol=1e-12)
+
+
+def _fd_batch(rng, n, vocab, rhos, advs):
+    zb = wl.f32_to_bf16_bits(rng.standard_normal((n, vocab)).astype(np.float32))
+    z = wl.bf16_bits_to_f32(zb).astype(np.float64)
+    tok = rng.integers(0, vocab, n).astype(np.int32)
+    m = np.ones(n, np.uint8)
+    lp = oracle.opd_loss(z, tok, np.zeros(n, np.float32), np.zeros(n, np.float32), m, [0, n])["lp"]
+    old = (lp - np.log(rhos)).astype(np.float32)
+    tea = (old.astype(np.float64) + advs).astype(np.float32)
+    return zb, z, tok, old, tea, m
+
+
+def test_opd_gradient_matches_finite_differences():
+    # rho values away from the kinks (0.8, 1.2, 3) cover every regime
+    rng = np.random.default_rng(5)
+    rhos = np.array([0.5, 1.05, 1.6, 0.6, 0.95, 2.0, 5.0, 1.1])
+    advs = np.array([0.7, 0.7, 0.7, -0.6, -0.6, -0.6, -0.6, 0.0])
+    n, vocab = len(rhos), 7
+    zb, z, tok, old, tea, m = _fd_batch(rng, n, vocab, rhos, advs)
+    st = [0, 3, 8]
+    base = oracle.opd_loss(zb, tok, old, tea, m, st)
+    grad = oracle.opd_grad_rows(zb, tok, m, base["dlp"], np.arange(n))
+    h = 1e-6
+    fd = np.zeros_like(z)
+    for j in range(n):
+        for v in range(vocab):
+            zp, zm = z.copy(), z.copy()
+            zp[j, v] += h
+            zm[j, v] -= h
+            fd[j, v] = (oracle.opd_loss(zp, tok, old, tea, m, st)["loss"]
+                        - oracle.opd_loss(zm, tok, old, tea, m, st)["loss"]) / (2 * h)
+    np.testing.assert_allclose(grad, fd, rtol=0, atol=1e-8)
+    assert np.abs(grad).max() > 1e-3  # some rows carry gradient
+    # flat regimes: no gradient at all
+    flat = [2, 3, 6, 7]
+    assert np.abs(grad[flat]).max() == 0
+
+
+def test_opd_logit_shift_invariance():
+    rng = np.random.default_rng(6)
+    zb, z, tok, old, tea, m = _fd_batch(rng, 6, 50, np.array([0.5, 1.1, 2.0, 0.9, 4.0, 1.3]),
+                                        np.array([0.3, -0.4, -0.2, 0.1, -0.5, 0.6]))
+    a = oracle.opd_loss(z, tok, old, tea, m, [0, 2, 6])
+    b = oracle.opd_loss(z + rng.standard_normal((6, 1)) * 10, tok, old, tea, m, [0, 2, 6])
+    np.testing.assert_allclose(b["lp"], a["lp"], atol=1e-12)
+    assert b["loss"] == pytest.approx(a["loss"], abs=1e-12)
+
+
+def test_opd_rejects_bad_inputs():
+    z = _one_hot_rows(2)
+    ok = dict(tokens=[0, 0], old_lp=[0, 0], tea_lp=[0, 0], mask=[1, 1], seq_starts=[0, 2])
+    oracle.opd_loss(z, **ok)
+    with pytest.raises(ValueError):
+        oracle.opd_loss(z, **{**ok, "tokens": [0, 4]})
+    with pytest.raises(ValueError):
+        oracle.opd_loss(z, **{**ok, "seq_starts": [0, 1]})
+    with pytest.raises(ValueError):
+        oracle.opd_loss(z, **{**ok, "seq_starts": [1, 2]})
+    oracle.opd_loss(z, **{**ok, "tokens": [0, 4], "mask": [1, 0]})  # masked rows are not read
