@@ -28,6 +28,7 @@ EXPORTS = (
     "ctx_decode_attn_run",
     "ctx_decode_attn_run_paged",
     "ctx_prefill_attn_run",
+    "ctx_opd_loss_run",
     "ctx_decode_attn_destroy",
     "ctx_decode_attn_status_string",
     "ctx_decode_attn_last_error",
@@ -45,6 +46,19 @@ class CtxDesc(ctypes.Structure):
         ("split_tokens", ctypes.c_int32),
         ("page_tokens", ctypes.c_int32),
     ]
+
+
+class OpdParams(ctypes.Structure):
+    """ctx_opd_loss_params; defaults are the paper's values (App. OPD Optimization)."""
+    _fields_ = [
+        ("log_ratio_clip", ctypes.c_float),
+        ("clip_delta", ctypes.c_float),
+        ("dual_clip", ctypes.c_float),
+        ("eps", ctypes.c_float),
+    ]
+
+    def __init__(self, log_ratio_clip=20.0, clip_delta=0.2, dual_clip=3.0, eps=1e-8):
+        super().__init__(log_ratio_clip, clip_delta, dual_clip, eps)
 
 
 class CtxError(RuntimeError):
@@ -78,6 +92,9 @@ def load_library(path: str | None = None):
     lib.ctx_decode_attn_run_paged.restype = ctypes.c_int
     lib.ctx_prefill_attn_run.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp, i32, i32, ctypes.c_float, vp, vp]
     lib.ctx_prefill_attn_run.restype = ctypes.c_int
+    lib.ctx_opd_loss_run.argtypes = [vp, ctypes.c_int64, i32, vp, vp, vp, vp, vp, i32, i32,
+                                     ctypes.POINTER(OpdParams), vp, vp, vp, vp, vp, ctypes.c_int64, vp]
+    lib.ctx_opd_loss_run.restype = ctypes.c_int
     lib.ctx_decode_attn_destroy.argtypes = [vp]
     lib.ctx_decode_attn_destroy.restype = ctypes.c_int
     lib.ctx_decode_attn_status_string.argtypes = [ctypes.c_int]
@@ -256,3 +273,67 @@ class DecodeAttention:
             self.close()
         except Exception:
             pass
+
+
+def opd_loss(logits, tokens, old_logp, teacher_logp, mask, seq_starts, params: OpdParams | None = None,
+             grad: bool = True, out: dict | None = None, stream=None) -> dict:
+    """Fused OPD token loss (ctx_opd_loss_run) over a packed batch.
+
+    logits bf16 [N, stride] (the last dimension may be a view wider than vocab:
+    pass `vocab` via logits.shape[1] unless `out["vocab"]` is given), tokens int32 [N],
+    old_logp / teacher_logp float32 [N], mask uint8 [N], seq_starts int32 [B + 1].
+    Returns a dict of device tensors: loss [1], token_logp, token_weight,
+    token_loss [N] and, with grad=True, grad_logits bf16 [N, vocab].  Tensors
+    given in `out` under those names are written in place (no allocation)."""
+    import torch
+
+    lib = load_library()
+    params = params or OpdParams()
+    n = tokens.shape[0]
+    dev = logits.device
+    for name, t, dt in (("logits", logits, torch.bfloat16), ("tokens", tokens, torch.int32),
+                        ("old_logp", old_logp, torch.float32), ("teacher_logp", teacher_logp, torch.float32),
+                        ("mask", mask, torch.uint8), ("seq_starts", seq_starts, torch.int32)):
+        if t.dtype != dt:
+            raise TypeError(f"{name} must be {dt}, got {t.dtype}")
+        if not t.is_cuda or t.device != dev:
+            raise ValueError(f"{name} must be on {dev}")
+    if logits.dim() != 2 or logits.shape[0] != n or logits.stride(1) != 1:
+        raise ValueError("logits must be [N, V] with unit column stride")
+    for name, t in (("tokens", tokens), ("old_logp", old_logp), ("teacher_logp", teacher_logp),
+                    ("mask", mask), ("seq_starts", seq_starts)):
+        if not t.is_contiguous() or t.dim() != 1:
+            raise ValueError(f"{name} must be a contiguous vector")
+    out = dict(out or {})
+    vocab = int(out.pop("vocab", logits.shape[1]))
+
+    def buf(name, shape, dtype):
+        t = out.get(name)
+        if t is None:
+            t = torch.empty(shape, dtype=dtype, device=dev)
+        elif t.dtype != dtype or tuple(t.shape) != tuple(shape) or not t.is_contiguous() or t.device != dev:
+            raise ValueError(f"out[{name!r}] must be a contiguous {dtype} tensor of shape {tuple(shape)}")
+        return t
+
+    res = {"loss": buf("loss", (1,), torch.float32), "token_logp": buf("token_logp", (n,), torch.float32),
+           "token_weight": buf("token_weight", (n,), torch.float32),
+           "token_loss": buf("token_loss", (n,), torch.float32)}
+    g = None
+    if grad:
+        g = out.get("grad_logits")
+        if g is None:  # rows padded to a multiple of 8 elements (16-byte chunks)
+            g = torch.empty((n, (vocab + 7) // 8 * 8), dtype=torch.bfloat16, device=dev)
+        elif g.dtype != torch.bfloat16 or g.dim() != 2 or g.shape[0] != n or g.stride(1) != 1:
+            raise ValueError("out['grad_logits'] must be bf16 [N, >= vocab] with unit column stride")
+        res["grad_logits"] = g if out.get("grad_logits") is not None else g[:, :vocab]
+    if stream is None:
+        stream = torch.cuda.current_stream(dev)
+    sp = stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream)
+    rc = lib.ctx_opd_loss_run(logits.data_ptr(), logits.stride(0), vocab, tokens.data_ptr(), old_logp.data_ptr(),
+                              teacher_logp.data_ptr(), mask.data_ptr(), seq_starts.data_ptr(),
+                              seq_starts.shape[0] - 1, n, ctypes.byref(params), res["token_logp"].data_ptr(),
+                              res["token_weight"].data_ptr(), res["token_loss"].data_ptr(), res["loss"].data_ptr(),
+                              g.data_ptr() if g is not None else None, g.stride(0) if g is not None else 0, sp)
+    if rc != CTX_OK:
+        raise error_for(lib, rc)
+    return res

@@ -9,6 +9,7 @@ import sys
 PKG = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(PKG)
 SRC = os.path.join(PKG, "csrc", "ctx_decode_attn.hip")
+SRCS = [SRC, os.path.join(PKG, "csrc", "ctx_opd_loss.hip")]
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "libctx_decode_attn.so")
 ARCH = "gfx950"
@@ -34,7 +35,7 @@ def compile_flags() -> list[str]:
 
 def build(verbose: bool = False, extra: list[str] | None = None, out: str | None = None) -> str:
     out = out or LIB
-    cmd = [hipcc(), *compile_flags(), *(extra or []), "-shared", "-o", out + ".tmp", SRC]
+    cmd = [hipcc(), *compile_flags(), *(extra or []), "-shared", "-o", out + ".tmp", *SRCS]
     if verbose:
         print(" ".join(cmd), flush=True)
     res = subprocess.run(cmd, capture_output=True, text=True)

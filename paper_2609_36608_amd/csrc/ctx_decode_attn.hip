@@ -925,6 +925,15 @@ int64_t round_up(int64_t x, int64_t m) { return (x + m - 1) / m * m; }
 
 }  // namespace
 
+// The last-error message is shared with the library's other entry points
+// (the OPD loss), which report through these two functions.
+__attribute__((visibility("hidden"))) int ctx_report_error(int code, const char* msg) {
+  snprintf(g_last_error, sizeof g_last_error, "%s", msg);
+  return code;
+}
+
+__attribute__((visibility("hidden"))) void ctx_clear_error() { g_last_error[0] = '\0'; }
+
 struct ctx_decode_attn {
   ctx_decode_attn_desc desc;
   int device;

@@ -31,7 +31,7 @@ DEFAULT_SEED = 42
 HEAD_DIM = 128
 
 # tensor ids used in spawn keys
-_T_Q, _T_K, _T_V, _T_MASK, _T_LEN, _T_EXTRA, _T_LAYOUT, _T_DEVICE = range(8)
+_T_Q, _T_K, _T_V, _T_MASK, _T_LEN, _T_EXTRA, _T_LAYOUT, _T_DEVICE, _T_OPD, _T_OPD_LOGITS = range(10)
 
 BF16_NAN = np.uint16(0x7FC0)
 
@@ -285,3 +285,109 @@ def fill_normal_bf16_device(t, seed: int, *key: int) -> None:
     for s in range(0, flat.numel(), chunk):
         e = min(s + chunk, flat.numel())
         flat[s:e].normal_(generator=g)
+
+
+# ----------------------------------------------------------------- OPD loss batches
+# An optimization batch of turn-level full responses (App. OPD Optimization;
+# tab:training-hyperparameters: 64 responses per batch, full-response limit 512
+# tokens, Qwen3 students with a 151,936-entry vocabulary, bf16).  Half of the
+# responses carry an inserted span (the thinking-budget close, App. thinking)
+# that stays in the context but is not supervised.
+
+
+@dataclass(frozen=True)
+class OpdWorkload:
+    name: str
+    index: int
+    responses: int
+    length_lo: int
+    length_hi: int
+    vocab: int
+    row_stride: int
+    logit_std: float = 2.0
+    inserted_frac: float = 0.5    # responses with an inserted (masked) span
+    inserted_len: int = 8
+    outlier_frac: float = 0.03    # tokens whose stored log-probability is far off
+    description: str = field(default="", compare=False)
+
+
+OPD_WORKLOADS = {
+    "opd_tiny": OpdWorkload("opd_tiny", 20, responses=6, length_lo=0, length_hi=48, vocab=1003,
+                            row_stride=1008, inserted_len=4, outlier_frac=0.2,
+                            description="6 responses of U{0..48} tokens, vocabulary 1,003 in rows of 1,008"),
+    "opd_qwen3": OpdWorkload("opd_qwen3", 21, responses=64, length_lo=64, length_hi=512, vocab=151936,
+                             row_stride=151936,
+                             description="OPD batch: 64 turn-level full responses of U{64..512} tokens, "
+                                         "Qwen3 vocabulary 151,936, bf16 logits N(0, 2^2)"),
+}
+
+
+@dataclass
+class OpdBatch:
+    seq_starts: np.ndarray   # int32 [B + 1]
+    tokens: np.ndarray       # int32 [N] sampled tokens
+    mask: np.ndarray         # uint8 [N] 1 = supervised
+    lp_target: np.ndarray    # float64 [N] where the student's log-probability of the token is placed
+    old_lp: np.ndarray       # float32 [N] stored sampling log-probabilities
+    teacher_lp: np.ndarray   # float32 [N] teacher log-probabilities
+
+    @property
+    def num_tokens(self) -> int:
+        return int(self.seq_starts[-1])
+
+
+def opd_batch(w: OpdWorkload, seed: int = DEFAULT_SEED) -> OpdBatch:
+    """Lengths, masks, tokens and the stored log-probabilities of a batch.
+    The sampled token's log-probability is drawn from -Exp(1); the stored one
+    is that plus N(0, 0.1^2), with outlier_frac of the tokens moved by
+    +-U(1, 30) (stale samples, exercising every clipping regime); the teacher's
+    is the stored one plus N(0, 1)."""
+    rng = rng_for(seed, w.index, 0, _T_OPD)
+    lens = rng.integers(w.length_lo, w.length_hi + 1, size=w.responses)
+    starts = np.concatenate([[0], np.cumsum(lens)]).astype(np.int32)
+    n = int(starts[-1])
+    mask = np.ones(n, np.uint8)
+    for b in range(w.responses):
+        if lens[b] > w.inserted_len and rng.random() < w.inserted_frac:
+            pos = int(rng.integers(0, lens[b] - w.inserted_len + 1))
+            mask[starts[b] + pos: starts[b] + pos + w.inserted_len] = 0
+    tokens = rng.integers(0, w.vocab, size=n).astype(np.int32)
+    lp_target = -rng.exponential(1.0, size=n)
+    old = lp_target + rng.normal(0.0, 0.1, size=n)
+    out = rng.random(n) < w.outlier_frac
+    old[out] += rng.choice([-1.0, 1.0], size=int(out.sum())) * rng.uniform(1.0, 30.0, size=int(out.sum()))
+    teacher = old + rng.normal(0.0, 1.0, size=n)
+    return OpdBatch(starts, tokens, mask, lp_target, old.astype(np.float32), teacher.astype(np.float32))
+
+
+def _opd_token_logit(w: OpdWorkload, batch: OpdBatch) -> np.ndarray:
+    # an N(0, s^2) row of V logits has log-sum-exp close to log V + s^2 / 2;
+    # the sampled token's logit goes that far above its target log-probability
+    return batch.lp_target + math.log(w.vocab) + 0.5 * w.logit_std ** 2
+
+
+def opd_logits_host(w: OpdWorkload, batch: OpdBatch, seed: int = DEFAULT_SEED) -> np.ndarray:
+    """bf16 bits [N, row_stride]: N(0, s^2) logits with the sampled token placed;
+    columns >= vocab and masked rows hold NaN (never read)."""
+    rng = rng_for(seed, w.index, 1, _T_OPD_LOGITS)
+    n = batch.num_tokens
+    z = rng.standard_normal((n, w.row_stride), dtype=np.float32) * np.float32(w.logit_std)
+    z[np.arange(n), batch.tokens] = _opd_token_logit(w, batch).astype(np.float32)
+    z[:, w.vocab:] = np.nan
+    z[batch.mask == 0] = np.nan
+    return f32_to_bf16_bits(z)
+
+
+def opd_logits_device(w: OpdWorkload, batch: OpdBatch, device, seed: int = DEFAULT_SEED):
+    """The same kind of logits drawn on the device (full-size batches): bf16
+    [N, row_stride] torch tensor, every entry finite."""
+    import torch
+
+    n = batch.num_tokens
+    t = torch.empty((n, w.row_stride), dtype=torch.bfloat16, device=device)
+    fill_normal_bf16_device(t, seed, w.index, 1, _T_OPD_LOGITS)
+    t.mul_(w.logit_std)
+    rows = torch.arange(n, device=device)
+    cols = torch.from_numpy(batch.tokens.astype(np.int64)).to(device)
+    t[rows, cols] = torch.from_numpy(_opd_token_logit(w, batch).astype(np.float32)).to(device).to(torch.bfloat16)
+    return t
