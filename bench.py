@@ -48,14 +48,16 @@ def profiled_traffic(workload: str, kernel: str = "decode_split_kernel"):
     import glob
     import hashlib
 
-    src = os.path.join(ROOT, "paper_2609_36608_amd", "csrc", "ctx_decode_attn.hip")
-    digest = hashlib.sha256(open(src, "rb").read()).hexdigest()
     for path in glob.glob(os.path.join(ROOT, "profiles", "*hbm_traffic*.md")):
         fields = {}
         for line in open(path):
             if ":" in line and not line.startswith(("|", "#", "`")):
                 k, _, v = line.partition(":")
                 fields[k.strip()] = v.strip()
+        src = os.path.join(ROOT, fields.get("kernel_source", "paper_2609_36608_amd/csrc/ctx_decode_attn.hip"))
+        if not os.path.exists(src):
+            continue
+        digest = hashlib.sha256(open(src, "rb").read()).hexdigest()
         if (fields.get("kernel_source_sha256") == digest and fields.get("workload") == workload
                 and fields.get("kernel", "decode_split_kernel") == kernel):
             t = int(fields["traffic_bytes_per_launch"])
@@ -279,6 +281,146 @@ def bench_prefill(args) -> int:
     return 0
 
 
+OPD_METRIC = "fused OPD token loss + logits gradient HBM GB/s (fraction of 8 TB/s peak), 1 MI355X"
+
+
+def opd_bytes(b: wl.OpdBatch, vocab: int, grad: bool = True) -> int:
+    """Bytes a call must move at least: every supervised logits row read once,
+    every gradient row written once (masked rows: zeros), the per-token inputs
+    (token, two log-probabilities, mask) and outputs (lp, weight, loss)."""
+    n = b.num_tokens
+    sup = int(b.mask.sum())
+    return sup * vocab * 2 + (n * vocab * 2 if grad else 0) + n * (4 + 4 + 4 + 1) + n * 12 + 4 * len(b.seq_starts)
+
+
+def opd_cpu_baseline(w, b: wl.OpdBatch, z_host_fn, target_s: float, threads: int) -> dict:
+    """The CPU oracle (loss over a sub-batch of whole responses, then the
+    gradient rows of those tokens), repeated for about target_s seconds."""
+    import oracle
+
+    r = 4
+    end = int(b.seq_starts[r])
+    sub = wl.OpdBatch(b.seq_starts[:r + 1].copy(), b.tokens[:end], b.mask[:end], b.lp_target[:end],
+                      b.old_lp[:end], b.teacher_lp[:end])
+    zh = z_host_fn(end)
+    nbytes = opd_bytes(sub, w.vocab)
+    reps, t0 = 0, time.perf_counter()
+    while True:
+        ref = oracle.opd_loss(zh, sub.tokens, sub.old_lp, sub.teacher_lp, sub.mask, sub.seq_starts, threads=threads)
+        oracle.opd_grad_rows(zh, sub.tokens, sub.mask, ref["dlp"], np.arange(end), threads=threads)
+        reps += 1
+        el = time.perf_counter() - t0
+        if el >= target_s or el / reps * (reps + 1) > 3 * target_s:
+            break
+    return {
+        "value": round(nbytes * reps / el / 1e9, 4),
+        "unit": "GB/s",
+        "cores": threads,
+        "kind": "oracle",
+        "sample": (f"responses 0..{r - 1} of {w.responses} ({end} tokens x {w.vocab} logits): loss, per-token "
+                   f"values and every gradient row, run {reps}x in {el:.1f} s; float64 C oracle, OpenMP over tokens"),
+    }
+
+
+def bench_opd(args) -> int:
+    """Per step one ctx_opd_loss_run over a full OPD batch: loss, per-token
+    values and the bf16 logits gradient."""
+    import torch
+
+    from paper_2609_36608_amd import binding
+
+    if not torch.cuda.is_available():
+        print("bench.py: no GPU visible", file=sys.stderr)
+        return 1
+    dev = torch.device("cuda", 0)
+    torch.cuda.set_device(dev)
+    w = wl.OPD_WORKLOADS["opd_qwen3"]
+    b = wl.opd_batch(w)
+    n = b.num_tokens
+    t_setup = time.perf_counter()
+    z = wl.opd_logits_device(w, b, dev)
+    up = lambda a, dt: torch.from_numpy(np.ascontiguousarray(a)).to(dev).to(dt)  # noqa: E731
+    tok, old, tea = up(b.tokens, torch.int32), up(b.old_lp, torch.float32), up(b.teacher_lp, torch.float32)
+    msk, st = up(b.mask, torch.uint8), up(b.seq_starts, torch.int32)
+    out = {"grad_logits": torch.empty((n, w.row_stride), dtype=torch.bfloat16, device=dev),
+           "loss": torch.empty(1, dtype=torch.float32, device=dev),
+           "token_logp": torch.empty(n, dtype=torch.float32, device=dev),
+           "token_weight": torch.empty(n, dtype=torch.float32, device=dev),
+           "token_loss": torch.empty(n, dtype=torch.float32, device=dev)}
+    torch.cuda.synchronize()
+    setup_s = time.perf_counter() - t_setup
+    stream = torch.cuda.current_stream()
+
+    def step() -> None:
+        binding.opd_loss(z, tok, old, tea, msk, st, out=out, stream=stream)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    start = torch.cuda.Event(enable_timing=True)
+    stop = torch.cuda.Event(enable_timing=True)
+    start.record(stream)
+    for _ in range(args.steps):
+        step()
+    stop.record(stream)
+    stop.synchronize()
+    torch.cuda.synchronize()
+    elapsed_s = start.elapsed_time(stop) / 1e3
+    if args.calibrate_copy_gib > 0:
+        ncopy = int(args.calibrate_copy_gib * 2**30) // 4
+        src = torch.ones(ncopy, dtype=torch.float32, device=dev)
+        dst = torch.empty_like(src)
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
+    nbytes = opd_bytes(b, w.vocab)
+    call_s = elapsed_s / args.steps
+    gbs = nbytes / call_s / 1e9
+    result = {
+        "metric": OPD_METRIC,
+        "value": round(gbs, 2),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(call_s * 1e3, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {
+            "workload": w.description,
+            "name": w.name,
+            "tokens": n,
+            "supervised_tokens": int(b.mask.sum()),
+            "vocab": w.vocab,
+            "seed": wl.DEFAULT_SEED,
+            "parallelism": "none (1 GPU)",
+        },
+        "frac_of_hbm_peak": round(gbs / HBM_PEAK_GBS, 4),
+        "tokens_per_s": round(n / call_s, 1),
+        "roofline": {
+            "bound": "hbm",
+            "achieved": round(gbs, 2),
+            "peak": HBM_PEAK_GBS,
+            "unit": "GB/s",
+            "frac": round(gbs / HBM_PEAK_GBS, 4),
+            "traffic": profiled_traffic(w.name, "opd_row_kernel"),
+            "kernel": "opd_row_kernel (+ opd_weight_kernel, opd_reduce_kernel: one ctx_opd_loss_run call)",
+            "bytes_per_launch": nbytes,
+            "avg_launch_us": round(call_s * 1e6, 3),
+        },
+        "setup_s": round(setup_s, 1),
+    }
+    if not args.no_cpu_baseline:
+        threads = len(os.sched_getaffinity(0))
+        zfn = lambda rows: z[:rows].view(torch.int16).cpu().numpy().view(np.uint16)  # noqa: E731
+        result["cpu_baseline"] = opd_cpu_baseline(w, b, zfn, args.cpu_seconds, threads)
+    print(json.dumps(result), flush=True)
+    return 0
+
+
 def main() -> int:
     ap = argparse.ArgumentParser(description=__doc__)
     ap.add_argument("--gpus", type=int, default=1)
@@ -291,6 +433,8 @@ def main() -> int:
     ap.add_argument("--prefill", action="store_true",
                     help="time the causal prefill of the appended reference observation instead "
                          "(act_first_burst)")
+    ap.add_argument("--opd", action="store_true",
+                    help="time the fused OPD token loss + logits gradient instead (64 responses, Qwen3 vocabulary)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--calibrate-copy-gib", type=float, default=0.0,
@@ -308,6 +452,8 @@ def main() -> int:
 
     if args.prefill:
         return bench_prefill(args)
+    if args.opd:
+        return bench_opd(args)
 
     import torch
 

@@ -12,17 +12,18 @@
 // Design:
 //   * opd_weight_kernel: one workgroup per response counts its supervised
 //     tokens and writes w_j = m_j / (B (M_b + eps)).
-//   * opd_row_kernel<C>: one 1024-thread workgroup per token row holds the
-//     whole row in registers (thread t owns the 16-byte chunks t + 1024 k,
-//     k < C: coalesced, non-temporal loads).  It reduces the row maximum and
+//   * opd_row_kernel<C>: a persistent 1024-thread workgroup per CU walks the
+//     token rows; it holds a whole row in registers (thread t owns the
+//     16-byte chunks t + 1024 k, k < C: coalesced, non-temporal loads).  It reduces the row maximum and
 //     the sum of exp over the registers (wave shuffles, then 16 partials
 //     through LDS, always in the same order), forms lp, the clipped ratio,
 //     the dual-clip loss and the per-row gradient scale g, and writes the
 //     gradient row g (onehot - softmax) from the same registers, rounded to
 //     bf16.  A row whose g is 0 (a flat clipping regime or A = 0) writes
 //     zeros without the second exp pass; a masked row is not read at all.
-//     With ~100 VGPRs a CU holds one such workgroup; the 256 CUs drift out of
-//     phase, so loads of some rows overlap stores and math of others.
+//     At 128 VGPRs a CU holds one such workgroup, so the next row's loads are
+//     issued chunk by chunk as the gradient pass frees the registers: its
+//     HBM reads overlap this row's exps and gradient stores.
 //   * opd_reduce_kernel: loss = sum_j w_j l_j in double precision, one
 //     workgroup, fixed order (deterministic, no atomics).
 
@@ -157,134 +158,186 @@ __device__ __forceinline__ void dual_clip_loss(float rho, float a, const OpdPara
   *dloss = d;
 }
 
+// Buffer resource over `bytes` bytes from a wave-uniform base: loads past
+// the end return zeros and stores past it are dropped.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t row_rsrc(const void* base, uint32_t bytes) {
+  const uint64_t a = reinterpret_cast<uint64_t>(base);
+  const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)a);
+  const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(a >> 32));
+  const uint64_t u = ((uint64_t)hi << 32) | lo;
+  return __builtin_amdgcn_make_buffer_rsrc(reinterpret_cast<void*>(u), (short)0,
+                                           (int)__builtin_amdgcn_readfirstlane(bytes), 0x00020000);
+}
+
+constexpr int kNonTemporal = 2;  // buffer cache-policy bits: streamed once
+// Chunk offsets go in the VGPR offset, which the buffer range check covers;
+// the SGPR offset stays 0.
+constexpr int kWaitVmcnt0 = 0x0F70;  // s_waitcnt vmcnt(0), expcnt and lgkmcnt left open
+
+// An empty asm that "may change" every chunk of the row: the compiler then
+// recomputes the cheap bf16 -> fp32 unpacking in each pass instead of keeping
+// eight unpacked floats per chunk alive across passes (two rows' worth of
+// registers).  It emits no instruction.
+template <int C>
+__device__ __forceinline__ void opaque(u32x4 (&x)[C]) {
+#pragma unroll
+  for (int k = 0; k < C; ++k) asm volatile("" : "+v"(x[k]));
+}
+
 template <int C>
 __global__ __launch_bounds__(kRowThreads) void opd_row_kernel(
-    const uint16_t* __restrict__ logits, int64_t row_stride, int32_t vocab,
+    const uint16_t* __restrict__ logits, int64_t row_stride, int32_t vocab, int32_t num_rows,
     const int32_t* __restrict__ tokens, const float* __restrict__ old_logp,
     const float* __restrict__ teacher_logp, const uint8_t* __restrict__ mask,
     const float* __restrict__ weight, OpdParams prm, float* __restrict__ token_logp,
     float* __restrict__ token_loss, uint16_t* __restrict__ grad, int64_t grad_stride) {
   __shared__ float red[kRowWaves];
-  const int j = blockIdx.x;
   const int tid = threadIdx.x;
   const int nchunks = (vocab + kChunk - 1) / kChunk;
-  uint16_t* grow = grad != nullptr ? grad + (size_t)j * grad_stride : nullptr;
+  const int nwhole = vocab / kChunk;  // chunks with 8 columns below vocab
+  // C = ceil(nchunks / 1024): rounds k < C - 1 give every thread a whole
+  // chunk; only the last round tests chunks and columns against vocab
+  constexpr int kwhole = C - 1;
+  const uint32_t load_bytes = (uint32_t)nchunks * 16u;   // loads: every chunk (the partial one padded)
+  const uint32_t store_bytes = (uint32_t)nwhole * 16u;   // stores: whole chunks; a partial one apart
+  const int voff = tid * 16;
 
-  if (!mask[j]) {  // no loss, no gradient, logits not read
-    if (tid == 0) {
+  // Persistent: rows blockIdx.x, + gridDim.x, ...  The row is held in x; the
+  // next row's loads are issued chunk by chunk as the gradient pass frees x.
+  u32x4 x[C];
+  int j = blockIdx.x;
+  if (j >= num_rows) return;
+  bool sup = mask[j] != 0;
+  if (sup) {
+    const __amdgpu_buffer_rsrc_t rr = row_rsrc(logits + (size_t)j * row_stride, load_bytes);
+#pragma unroll
+    for (int k = 0; k < C; ++k)
+      x[k] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rr, voff + k * kRowThreads * 16, 0,
+                                                                              kNonTemporal));
+  }
+#pragma nounroll
+  for (; j < num_rows; j += gridDim.x) {
+    // per-row copy of the lane index, opaque to the compiler: lane-dependent
+    // masks and offsets are recomputed per row (a few instructions) instead of
+    // being hoisted out of the row loop, where they would occupy registers
+    int t = tid;
+    asm volatile("" : "+v"(t));
+    const int vo = t * 16;
+    const int jn = j + (int)gridDim.x;
+    const bool next_sup = jn < num_rows && mask[jn] != 0;
+    float g = 0.f, lse2 = 0.f;
+    int tok = -1;
+    if (sup) {
+      float mx = -INFINITY;
+#pragma unroll
+      for (int k = 0; k < C; ++k) {
+        if (k < kwhole) {
+#pragma unroll
+          for (int i = 0; i < 4; ++i) mx = fmaxf(mx, fmaxf(lo_bf16(x[k][i]), hi_bf16(x[k][i])));
+        } else {
+          const int c0 = (t + k * kRowThreads) * kChunk;
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            if (c0 + 2 * i < vocab) mx = fmaxf(mx, lo_bf16(x[k][i]));
+            if (c0 + 2 * i + 1 < vocab) mx = fmaxf(mx, hi_bf16(x[k][i]));
+          }
+        }
+        __builtin_amdgcn_sched_barrier(0);  // chunk by chunk: bounded live ranges
+      }
+      const float m2 = block_max(mx, red) * kLog2e;
+      opaque(x);
+      float s = 0.f;
+#pragma unroll
+      for (int k = 0; k < C; ++k) {
+        if (k < kwhole) {
+#pragma unroll
+          for (int i = 0; i < 4; ++i)
+            s += __builtin_amdgcn_exp2f(fmaf(lo_bf16(x[k][i]), kLog2e, -m2)) +
+                 __builtin_amdgcn_exp2f(fmaf(hi_bf16(x[k][i]), kLog2e, -m2));
+        } else {
+          const int c0 = (t + k * kRowThreads) * kChunk;
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            if (c0 + 2 * i < vocab) s += __builtin_amdgcn_exp2f(fmaf(lo_bf16(x[k][i]), kLog2e, -m2));
+            if (c0 + 2 * i + 1 < vocab) s += __builtin_amdgcn_exp2f(fmaf(hi_bf16(x[k][i]), kLog2e, -m2));
+          }
+        }
+        __builtin_amdgcn_sched_barrier(0);
+      }
+      lse2 = m2 + __log2f(block_sum(s, red));  // log2 of sum_v exp(z_v)
+      opaque(x);
+
+      // per-token scalars (every thread computes them; they are uniform)
+      tok = tokens[j];
+      const bool tok_ok = tok >= 0 && tok < vocab;
+      const float zt = tok_ok ? __uint_as_float((uint32_t)logits[(size_t)j * row_stride + tok] << 16)
+                              : __builtin_nanf("");
+      const float lp = zt - lse2 * kLn2;
+      const float old = old_logp[j];
+      const float a = teacher_logp[j] - old;
+      const float r = lp - old;
+      const float rc = fminf(fmaxf(r, -prm.clip_log), prm.clip_log);
+      const float rho = expf(rc);
+      const float drho = (r > -prm.clip_log && r < prm.clip_log) ? rho : 0.f;
+      float l, dl;
+      dual_clip_loss(rho, a, prm, &l, &dl);
+      g = weight[j] * dl * drho;
+      if (t == 0) {
+        if (token_logp != nullptr) token_logp[j] = lp;
+        token_loss[j] = l;
+      }
+    } else if (t == 0) {  // no loss, no gradient, logits not read
       if (token_logp != nullptr) token_logp[j] = 0.f;
       token_loss[j] = 0.f;
     }
-    if (grow != nullptr) {
-      const u32x4 z = {0u, 0u, 0u, 0u};
-#pragma unroll
-      for (int k = 0; k < C; ++k) {
-        const int q = tid + k * kRowThreads;
-        if (q < nchunks) store_chunk(grow, q, z, vocab);
-      }
-    }
-    return;
-  }
 
-  // the row, 16 bytes per chunk, straight into registers
-  const uint16_t* row = logits + (size_t)j * row_stride;
-  u32x4 x[C];
-#pragma unroll
-  for (int k = 0; k < C; ++k) {
-    const int q = tid + k * kRowThreads;
-    x[k] = q < nchunks ? __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(row) + q)
-                       : u32x4{0u, 0u, 0u, 0u};
-  }
-  // value e of chunk k is valid if its column is below vocab
-  auto valid = [&](int k, int e) { return (tid + k * kRowThreads) * kChunk + e < vocab; };
-
-  float mx = -INFINITY;
-#pragma unroll
-  for (int k = 0; k < C; ++k) {
-    if (tid + k * kRowThreads < nchunks) {
-      if ((tid + k * kRowThreads + 1) * kChunk <= vocab) {
-#pragma unroll
-        for (int i = 0; i < 4; ++i) mx = fmaxf(mx, fmaxf(lo_bf16(x[k][i]), hi_bf16(x[k][i])));
-      } else {
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          if (valid(k, 2 * i)) mx = fmaxf(mx, lo_bf16(x[k][i]));
-          if (valid(k, 2 * i + 1)) mx = fmaxf(mx, hi_bf16(x[k][i]));
-        }
-      }
-    }
-  }
-  const float row_max = block_max(mx, red);
-  const float m2 = row_max * kLog2e;
-
-  float s = 0.f;
-#pragma unroll
-  for (int k = 0; k < C; ++k) {
-    if (tid + k * kRowThreads < nchunks) {
-      if ((tid + k * kRowThreads + 1) * kChunk <= vocab) {
-#pragma unroll
-        for (int i = 0; i < 4; ++i)
-          s += __builtin_amdgcn_exp2f(fmaf(lo_bf16(x[k][i]), kLog2e, -m2)) +
-               __builtin_amdgcn_exp2f(fmaf(hi_bf16(x[k][i]), kLog2e, -m2));
-      } else {
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          if (valid(k, 2 * i)) s += __builtin_amdgcn_exp2f(fmaf(lo_bf16(x[k][i]), kLog2e, -m2));
-          if (valid(k, 2 * i + 1)) s += __builtin_amdgcn_exp2f(fmaf(hi_bf16(x[k][i]), kLog2e, -m2));
-        }
-      }
-    }
-  }
-  const float sum = block_sum(s, red);
-  const float lse2 = m2 + __log2f(sum);  // log2 of sum_v exp(z_v)
-
-  // per-token scalars (every thread computes them; they are wave-uniform)
-  const int tok = tokens[j];
-  const bool tok_ok = tok >= 0 && tok < vocab;
-  const float zt = tok_ok ? __uint_as_float((uint32_t)row[tok] << 16) : __builtin_nanf("");
-  const float lp = zt - lse2 * kLn2;
-  const float old = old_logp[j];
-  const float a = teacher_logp[j] - old;
-  const float r = lp - old;
-  const float rc = fminf(fmaxf(r, -prm.clip_log), prm.clip_log);
-  const float rho = expf(rc);
-  const float drho = (r > -prm.clip_log && r < prm.clip_log) ? rho : 0.f;
-  float l, dl;
-  dual_clip_loss(rho, a, prm, &l, &dl);
-  const float g = weight[j] * dl * drho;
-  if (tid == 0) {
-    if (token_logp != nullptr) token_logp[j] = lp;
-    token_loss[j] = l;
-  }
-  if (grow == nullptr) return;
-
-  // gradient row: g (onehot(tok) - exp(z - lse))
-  if (g == 0.f) {
-    const u32x4 z = {0u, 0u, 0u, 0u};
+    // gradient row g (onehot(tok) - exp(z - lse)); zeros when g = 0 (masked
+    // rows, flat clipping regimes); then the next row's chunk k into x[k]
+    const bool has_grad = grad != nullptr;
+    const __amdgpu_buffer_rsrc_t gr = row_rsrc(has_grad ? grad + (size_t)j * grad_stride : grad, store_bytes);
+    const __amdgpu_buffer_rsrc_t nr = row_rsrc(logits + (size_t)(next_sup ? jn : j) * row_stride, load_bytes);
+    const float ng = -g;
+    // Every load of this row has landed (the passes above read them); saying
+    // so here lets the compiler issue the chunk-by-chunk refills below without
+    // waiting on each other (on the masked-row path it could not tell).
+    __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
 #pragma unroll
     for (int k = 0; k < C; ++k) {
-      const int q = tid + k * kRowThreads;
-      if (q < nchunks) store_chunk(grow, q, z, vocab);
-    }
-    return;
-  }
-  const float ng = -g;
+      const int q = t + k * kRowThreads;
+      if (has_grad) {
+        u32x4 o = {0u, 0u, 0u, 0u};
+        if (g != 0.f) {
 #pragma unroll
-  for (int k = 0; k < C; ++k) {
-    const int q = tid + k * kRowThreads;
-    if (q < nchunks) {
-      u32x4 o;
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int c0 = q * kChunk + 2 * i;
-        float g0 = ng * __builtin_amdgcn_exp2f(fmaf(lo_bf16(x[k][i]), kLog2e, -lse2));
-        float g1 = ng * __builtin_amdgcn_exp2f(fmaf(hi_bf16(x[k][i]), kLog2e, -lse2));
-        if (c0 == tok) g0 += g;
-        if (c0 + 1 == tok) g1 += g;
-        o[i] = pack_bf16x2(g0, g1);
+          for (int i = 0; i < 4; ++i)
+            o[i] = pack_bf16x2(ng * __builtin_amdgcn_exp2f(fmaf(lo_bf16(x[k][i]), kLog2e, -lse2)),
+                               ng * __builtin_amdgcn_exp2f(fmaf(hi_bf16(x[k][i]), kLog2e, -lse2)));
+          if (q == tok / kChunk) {  // the sampled token's entry: g (1 - p)
+            const int e = tok - q * kChunk;
+            const uint32_t w = o[e >> 1];
+            const float zv = (e & 1) ? hi_bf16(x[k][e >> 1]) : lo_bf16(x[k][e >> 1]);
+            const float gv = fmaf(ng, __builtin_amdgcn_exp2f(fmaf(zv, kLog2e, -lse2)), g);
+            const uint32_t hv = pack_bf16x2(gv, gv) & 0xffffu;
+            o[e >> 1] = (e & 1) ? (w & 0xffffu) | (hv << 16) : (w & 0xffff0000u) | hv;
+          }
+        }
+        if (k < C - 1 || q < nwhole) {
+          __builtin_amdgcn_raw_buffer_store_b128(
+              __builtin_bit_cast(__attribute__((ext_vector_type(4))) unsigned, o), gr, vo + k * kRowThreads * 16, 0,
+              kNonTemporal);
+        } else if (q == nwhole && nwhole < nchunks) {  // the partial chunk: its columns below vocab
+          uint16_t* gp = grad + (size_t)j * grad_stride + (size_t)nwhole * kChunk;
+          for (int e = 0; e < vocab - nwhole * kChunk; ++e)
+            gp[e] = (uint16_t)(e & 1 ? o[e >> 1] >> 16 : o[e >> 1] & 0xffffu);
+        }
       }
-      store_chunk(grow, q, o, vocab);
+      if (next_sup)
+        x[k] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(nr, vo + k * kRowThreads * 16, 0,
+                                                                                kNonTemporal));
+      // keep the refill of x[k] after its last use: hoisting the loads would
+      // need a second row's worth of registers
+      __builtin_amdgcn_sched_barrier(0);
     }
+    sup = next_sup;
   }
 }
 
@@ -317,11 +370,11 @@ int fail(int code, const char* fmt, ...) {
 bool aligned16(const void* ptr) { return (reinterpret_cast<uintptr_t>(ptr) & 15u) == 0; }
 
 template <int C>
-void launch_rows(int32_t n, hipStream_t s, const uint16_t* logits, int64_t stride, int32_t vocab,
+void launch_rows(int32_t n, int grid, hipStream_t s, const uint16_t* logits, int64_t stride, int32_t vocab,
                  const int32_t* tokens, const float* old_lp, const float* tea_lp, const uint8_t* mask,
                  const float* weight, OpdParams prm, float* token_logp, float* token_loss, uint16_t* grad,
                  int64_t grad_stride) {
-  hipLaunchKernelGGL(opd_row_kernel<C>, dim3((unsigned)n), dim3(kRowThreads), 0, s, logits, stride, vocab,
+  hipLaunchKernelGGL(opd_row_kernel<C>, dim3((unsigned)grid), dim3(kRowThreads), 0, s, logits, stride, vocab, n,
                      tokens, old_lp, tea_lp, mask, weight, prm, token_logp, token_loss, grad, grad_stride);
 }
 
@@ -365,18 +418,38 @@ extern "C" int ctx_opd_loss_run(const void* logits, int64_t row_stride, int32_t 
     hipLaunchKernelGGL(opd_weight_kernel, dim3((unsigned)num_seqs), dim3(256), 0, s, mask, seq_starts, num_seqs,
                        p.eps, token_weight);
     const int64_t per_thread = ((int64_t)vocab + kChunk * kRowThreads - 1) / (kChunk * kRowThreads);
+    // one resident workgroup per CU (about 128 VGPRs x 16 waves fill it)
+    int device = 0, cus = 0;
+    hipError_t e = hipGetDevice(&device);
+    if (e == hipSuccess) e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, device);
+    if (e != hipSuccess) return fail(CTX_ERR_HIP, "device query: %s", hipGetErrorString(e));
+    const int grid = num_tokens < cus ? num_tokens : cus;
     const uint16_t* lg = static_cast<const uint16_t*>(logits);
     uint16_t* gr = static_cast<uint16_t*>(grad_logits);
 #define CTX_OPD_ROWS(C)                                                                                 \
-  launch_rows<C>(num_tokens, s, lg, row_stride, vocab, tokens, old_logp, teacher_logp, mask, token_weight, \
+  launch_rows<C>(num_tokens, grid, s, lg, row_stride, vocab, tokens, old_logp, teacher_logp, mask, token_weight, \
                  prm, token_logp, token_loss, gr, grad_row_stride)
-    if (per_thread <= 1) CTX_OPD_ROWS(1);
-    else if (per_thread <= 2) CTX_OPD_ROWS(2);
-    else if (per_thread <= 4) CTX_OPD_ROWS(4);
-    else if (per_thread <= 8) CTX_OPD_ROWS(8);
-    else if (per_thread <= 12) CTX_OPD_ROWS(12);
-    else if (per_thread <= 16) CTX_OPD_ROWS(16);
-    else CTX_OPD_ROWS(19);
+    switch (per_thread) {  // exactly ceil(chunks / 1024) chunks per thread
+      case 1: CTX_OPD_ROWS(1); break;
+      case 2: CTX_OPD_ROWS(2); break;
+      case 3: CTX_OPD_ROWS(3); break;
+      case 4: CTX_OPD_ROWS(4); break;
+      case 5: CTX_OPD_ROWS(5); break;
+      case 6: CTX_OPD_ROWS(6); break;
+      case 7: CTX_OPD_ROWS(7); break;
+      case 8: CTX_OPD_ROWS(8); break;
+      case 9: CTX_OPD_ROWS(9); break;
+      case 10: CTX_OPD_ROWS(10); break;
+      case 11: CTX_OPD_ROWS(11); break;
+      case 12: CTX_OPD_ROWS(12); break;
+      case 13: CTX_OPD_ROWS(13); break;
+      case 14: CTX_OPD_ROWS(14); break;
+      case 15: CTX_OPD_ROWS(15); break;
+      case 16: CTX_OPD_ROWS(16); break;
+      case 17: CTX_OPD_ROWS(17); break;
+      case 18: CTX_OPD_ROWS(18); break;
+      default: CTX_OPD_ROWS(19); break;
+    }
 #undef CTX_OPD_ROWS
   }
   hipLaunchKernelGGL(opd_reduce_kernel, dim3(1), dim3(1024), 0, s, token_weight, token_loss, num_tokens, loss);

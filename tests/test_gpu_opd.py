@@ -58,10 +58,15 @@ def check_scalars(got, ref, b, what):
     assert got["loss"][0] == pytest.approx(ref["loss"], rel=LOSS_RTOL, abs=LOSS_ATOL), what
 
 
-def check_grad_rows(got_rows, ref_rows, dlp_rows, what):
+def check_grad_rows(got_rows, ref_rows, dlp_rows, what, rows=None, tokens=None):
     scale = np.maximum(np.abs(ref_rows).max(axis=1, keepdims=True), 1e-30)
     err = np.abs(got_rows - ref_rows)
     bad = err > GRAD_RTOL * np.abs(ref_rows) + 1e-5 * scale
+    if bad.any():
+        for i, c in list(zip(*np.nonzero(bad)))[:12]:
+            r = rows[i] if rows is not None else i
+            print(f"{what}: row {r} col {c} got {got_rows[i, c]:.4e} ref {ref_rows[i, c]:.4e} "
+                  f"dlp {dlp_rows[i]:.3e} token {tokens[r] if tokens is not None else '?'}", flush=True)
     assert not bad.any(), f"{what}: {bad.sum()} gradient entries off, worst {err.max():.3e}"
     assert np.isfinite(got_rows).all()
 
@@ -93,7 +98,7 @@ def test_opd_edge_batches():
     """Empty responses, a fully masked response, length-1 responses, a vocab
     below one chunk and one of exactly one chunk per thread round."""
     rng = np.random.default_rng(9)
-    for vocab, stride in [(7, 8), (8, 8), (8193, 8200), (4096, 4096)]:
+    for vocab, stride in [(7, 8), (8, 8), (8193, 8200), (4096, 4096), (50257, 50264)]:
         lens = np.array([0, 1, 5, 0, 3, 1])
         starts = np.concatenate([[0], np.cumsum(lens)]).astype(np.int32)
         n = int(starts[-1])
@@ -156,7 +161,7 @@ def test_opd_full_size_qwen3_batch():
     rows = np.sort(np.concatenate([rng.choice(ok, 10, replace=False), np.nonzero(b.mask == 0)[0][:2],
                                    np.nonzero(ref["dlp"] == 0)[0][:2]]))
     gref = oracle.opd_grad_rows(zh, b.tokens, b.mask, ref["dlp"], rows)
-    check_grad_rows(got["grad_logits"][rows], gref, ref["dlp"][rows], "opd_qwen3")
+    check_grad_rows(got["grad_logits"][rows], gref, ref["dlp"][rows], "opd_qwen3", rows, b.tokens)
     print(f"opd_qwen3: loss {got['loss'][0]:.6f} vs {ref['loss']:.6f}; "
           f"lp max err {np.abs(got['token_logp'] - ref['lp'])[b.mask == 1].max():.2e}", flush=True)
 
