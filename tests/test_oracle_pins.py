@@ -639,3 +639,128 @@ def test_opd_rejects_bad_inputs():
     with pytest.raises(ValueError):
         oracle.opd_loss(z, **{**ok, "seq_starts": [1, 2]})
     oracle.opd_loss(z, **{**ok, "tokens": [0, 4], "mask": [1, 0]})  # masked rows are not read
+
+
+# ---------------------------------------------------------------- rollout scheduler
+# Prop. 1 (eq:ideal-rollout-speedup), App. finite concurrency
+# (eq:finite-capacity-time-bound), the calibrated estimate
+# (eq:calibrated-rollout-speedup).
+
+from oracle import oracle_sched as sch  # noqa: E402
+
+
+def _uniform(n, turns, value):
+    return [[value] * turns for _ in range(n)]
+
+
+@pytest.mark.parametrize("n,turns,lf,lu", [(1, 1, 1.0, 8.0), (4, 30, 1.0, 8.0), (16, 8, 0.5, 2.0), (3, 5, 2.0, 2.0)])
+def test_sched_prop1_with_enough_slots(n, turns, lf, lu):
+    """With a slot for every request (2NT) no request waits: Vanilla takes
+    T l_full and ActFirst (T - 1) l_fast + l_full (Prop. 1).  (2N slots are not
+    enough: ActFirst keeps up to about l_full / l_fast full responses of a task
+    in flight.)"""
+    van = sch.simulate_latency(sch.VANILLA, _uniform(n, turns, lf), _uniform(n, turns, lu), 2 * n * turns)
+    act = sch.simulate_latency(sch.ACTFIRST, _uniform(n, turns, lf), _uniform(n, turns, lu), 2 * n * turns)
+    assert van["completion"] == pytest.approx(turns * lu)
+    assert act["completion"] == pytest.approx((turns - 1) * lf + lu)
+    s = van["completion"] / act["completion"]
+    assert s == pytest.approx(sch.ideal_speedup(turns, lf, lu))
+    assert 1.0 - 1e-12 <= s <= min(turns, lu / lf) + 1e-12
+
+
+def test_sched_ideal_speedup_values():
+    # T l_full / ((T-1) l_fast + l_full): by hand
+    assert sch.ideal_speedup(1, 1.0, 8.0) == 1.0
+    assert sch.ideal_speedup(30, 1.0, 8.0) == pytest.approx(240.0 / 37.0)
+    assert sch.ideal_speedup(10 ** 9, 1.0, 8.0) == pytest.approx(8.0, rel=1e-7)  # the T -> infinity limit
+    assert sch.ideal_speedup(4, 2.0, 2.0) == 1.0                                  # equal latencies: no gain
+
+
+def test_sched_calibrated_estimate():
+    """Per-task constant latencies, unrestricted overlap: the batch waits for
+    its slowest task (eq:calibrated-rollout-speedup), including a task whose
+    fast action is slower than its full response."""
+    lf = [1.0, 0.5, 3.0, 0.2]
+    lu = [4.0, 6.0, 2.0, 1.0]
+    turns = 7
+    fast = [[a] * turns for a in lf]
+    full = [[b] * turns for b in lu]
+    van = sch.simulate_latency(sch.VANILLA, fast, full, 1000)
+    act = sch.simulate_latency(sch.ACTFIRST, fast, full, 1000)
+    assert van["completion"] == pytest.approx(max(turns * b for b in lu))          # 42
+    assert act["completion"] == pytest.approx(max((turns - 1) * a + max(a, b) for a, b in zip(lf, lu)))  # 21
+    assert sch.calibrated_completion(sch.VANILLA, lf, lu, turns) == pytest.approx(42.0)
+    assert sch.calibrated_completion(sch.ACTFIRST, lf, lu, turns) == pytest.approx(21.0)
+
+
+def test_sched_schedule_by_hand():
+    """N = 2, T = 2, l_fast = 1, l_full = 3, FIFO admission (submission time,
+    task, turn, fast before full).  One slot: Vanilla serves 0/0 [0,3], 1/0
+    [3,6], 0/1 [6,9], 1/1 [9,12]; ActFirst serves 0/0 fast [0,1], 0/0 full
+    [1,4], 1/0 fast [4,5], 1/0 full [5,8], 0/1 fast [8,9], 0/1 full [9,12],
+    1/1 fast [12,13], 1/1 full [13,16].  Four slots: Vanilla 6; ActFirst admits
+    all four turn-0 requests at 0, task 0's turn-1 pair at 1 (two slots free),
+    task 1's turn-1 fast at 2 and its full at 3 -> 6.  Eight slots: 4."""
+    fast, full = _uniform(2, 2, 1.0), _uniform(2, 2, 3.0)
+    van = sch.simulate_latency(sch.VANILLA, fast, full, 1)
+    act = sch.simulate_latency(sch.ACTFIRST, fast, full, 1)
+    assert van["completion"] == 12.0 and act["completion"] == 16.0
+    assert [van["start"][(i, t, 1)] for i, t in [(0, 0), (1, 0), (0, 1), (1, 1)]] == [0.0, 3.0, 6.0, 9.0]
+    want = {(0, 0, 0): 0, (0, 0, 1): 1, (1, 0, 0): 4, (1, 0, 1): 5, (0, 1, 0): 8, (0, 1, 1): 9,
+            (1, 1, 0): 12, (1, 1, 1): 13}
+    assert {k: act["start"][k] for k in want} == {k: float(v) for k, v in want.items()}
+    assert sch.simulate_latency(sch.VANILLA, fast, full, 4)["completion"] == 6.0
+    a4 = sch.simulate_latency(sch.ACTFIRST, fast, full, 4)
+    assert a4["completion"] == 6.0
+    assert (a4["start"][(0, 1, 0)], a4["start"][(1, 1, 0)], a4["start"][(1, 1, 1)]) == (1.0, 2.0, 3.0)
+    assert sch.simulate_latency(sch.ACTFIRST, fast, full, 8)["completion"] == 4.0
+    assert act["peak"] == 1 and van["peak"] == 1
+
+
+def test_sched_finite_concurrency_bounds():
+    """For any cap, ActFirst's completion respects the dependency chain and the
+    slot-time bound (eq:finite-capacity-time-bound); the speedup respects
+    eq:finite-capacity-speedup; admitted requests never exceed the cap."""
+    rng = np.random.default_rng(8)
+    for _ in range(40):
+        n, turns = int(rng.integers(1, 6)), int(rng.integers(1, 7))
+        lf, lu = float(rng.uniform(0.1, 2)), float(rng.uniform(0.1, 5))
+        b = int(rng.integers(1, 2 * n + 2))
+        van = sch.simulate_latency(sch.VANILLA, _uniform(n, turns, lf), _uniform(n, turns, lu), b)
+        act = sch.simulate_latency(sch.ACTFIRST, _uniform(n, turns, lf), _uniform(n, turns, lu), b)
+        lower = sch.completion_lower_bound(n, turns, lf, lu, b)
+        assert act["completion"] >= lower - 1e-9
+        assert van["completion"] / act["completion"] <= van["completion"] / lower + 1e-9
+        assert act["peak"] <= b and van["peak"] <= b
+        # dependencies: a turn's requests start no earlier than the gating request of the turn before
+        for i in range(n):
+            for t in range(1, turns):
+                assert act["start"][(i, t, 0)] >= act["end"][(i, t - 1, 0)] - 1e-12
+                assert van["start"][(i, t, 1)] >= van["end"][(i, t - 1, 1)] - 1e-12
+
+
+@pytest.mark.parametrize("b_max", [1, 2, 3, 5, 100])
+def test_sched_engine_with_constant_steps_equals_latency_model(b_max):
+    """With a constant step cost the engine model reduces to the latency model
+    with l = output tokens x step, for any cap."""
+    rng = np.random.default_rng(b_max)
+    n, turns = 3, 4
+    ctx = [[int(rng.integers(10, 50)) for _ in range(turns)] for _ in range(n)]
+    for policy in (sch.VANILLA, sch.ACTFIRST):
+        e = sch.simulate_engine(policy, ctx, 2, 7, b_max, base=0.5, per_kv=0.0, prefill=0.0)
+        lat = sch.simulate_latency(policy, _uniform(n, turns, 1.0), _uniform(n, turns, 3.5), b_max)
+        assert e["completion"] == pytest.approx(lat["completion"])
+        for k, v in lat["start"].items():
+            assert e["start"][k] == pytest.approx(v)
+
+
+def test_sched_engine_by_hand():
+    """One task, one turn, context 4 tokens, fast 2 and full 3 output tokens,
+    step = 1 + 0.5 x KV tokens + 0.25 x newly prefilled tokens.
+    Vanilla: 1 + 0.5*4 + 0.25*4 = 4, then 1 + 0.5*5 = 3.5, then 1 + 0.5*6 = 4 -> 11.5.
+    ActFirst (both admitted at 0): 1 + 0.5*8 + 0.25*8 = 7, 1 + 0.5*10 = 6, 1 + 0.5*6 = 4 -> 17;
+    the fast action ends at 13."""
+    v = sch.simulate_engine(sch.VANILLA, [[4]], 2, 3, 8, base=1.0, per_kv=0.5, prefill=0.25)
+    a = sch.simulate_engine(sch.ACTFIRST, [[4]], 2, 3, 8, base=1.0, per_kv=0.5, prefill=0.25)
+    assert v["completion"] == 11.5 and v["steps"] == 3
+    assert a["completion"] == 17.0 and a["end"][(0, 0, 0)] == 13.0
