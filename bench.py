@@ -421,6 +421,165 @@ def bench_opd(args) -> int:
     return 0
 
 
+SIM_METRIC = ("simulated rollout speedup, ActFirst-OPD over think-then-act (16 tasks, T=30, b_max=256, "
+              "16-token fast actions, 512-token full responses), engine model with MI355X-measured attention cost")
+# Qwen3-1.7B, the student of the rollout-efficiency study: 28 layers, 16 query
+# and 8 KV heads of 128; about 1.72e9 bf16 parameters streamed once per decode step
+SIM_LAYERS, SIM_HQ, SIM_HKV, SIM_PARAMS = 28, 16, 8, 1.72e9
+COPY_CEILING_GBS = 7090.0   # measured streaming-read ceiling of this part (NT loads)
+
+
+def calibrate_attention(torch, dev):
+    """Time ctx_decode_attn_run at the Qwen3-1.7B shape for several batches and
+    context lengths; least-squares fit of seconds per call = a + b * KV tokens."""
+    from paper_2609_36608_amd.binding import DecodeAttention
+
+    pts = []
+    total_bytes, total_s = 0, 0.0
+    for batch, ctx in [(16, 2048), (64, 2048), (64, 4096), (128, 3072), (256, 2048), (256, 4096)]:
+        lens = np.full(batch, ctx, np.int32)
+        layout = wl.make_layout(lens, 1)
+        k = torch.empty((layout.num_rows, SIM_HKV, 128), dtype=torch.bfloat16, device=dev)
+        v = torch.empty_like(k)
+        wl.fill_normal_bf16_device(k, 7, batch, ctx, 1)
+        wl.fill_normal_bf16_device(v, 7, batch, ctx, 2)
+        q = torch.empty((batch, SIM_HQ, 128), dtype=torch.bfloat16, device=dev)
+        wl.fill_normal_bf16_device(q, 7, batch, ctx, 0)
+        out = torch.empty((batch, SIM_HQ, 128), dtype=torch.float32, device=dev)
+        offs = torch.from_numpy(layout.offsets).to(dev)
+        tl = torch.from_numpy(lens).to(dev)
+        with DecodeAttention(SIM_HQ, SIM_HKV, batch, ctx) as attn:
+            for _ in range(3):
+                attn.run(q, k, v, offs, tl, 0.0884, out)
+            torch.cuda.synchronize()
+            reps = 50
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            for _ in range(reps):
+                attn.run(q, k, v, offs, tl, 0.0884, out)
+            e1.record()
+            e1.synchronize()
+            sec = e0.elapsed_time(e1) / 1e3 / reps
+        pts.append((batch * ctx, sec))
+        w = wl.Workload("sim", 0, 1, batch, SIM_HQ, SIM_HKV, 1, "uniform", ctx, ctx)
+        total_bytes += algorithmic_bytes(lens, w) * reps
+        total_s += sec * reps
+        del k, v
+    x = np.array([p[0] for p in pts], np.float64)
+    y = np.array([p[1] for p in pts], np.float64)
+    b, a = np.polyfit(x, y, 1)
+    return {"per_call_s": float(a), "per_kv_token_s": float(b), "points": pts,
+            "achieved_gbs": total_bytes / total_s / 1e9, "avg_call_us": total_s / (len(pts) * 50) * 1e6,
+            "bytes_per_call": total_bytes / (len(pts) * 50)}
+
+
+def sim_contexts(n: int, turns: int, seed: int = wl.DEFAULT_SEED) -> np.ndarray:
+    """Fixed interaction contexts reused across the virtual turns (as in the
+    rollout-efficiency study): one ALFWorld-like prompt of U{1500..3000} tokens per task."""
+    rng = wl.rng_for(seed, 30, 0, 0)
+    return np.repeat(rng.integers(1500, 3001, size=n)[:, None], turns, axis=1).astype(np.int32)
+
+
+def bench_sim(args) -> int:
+    """Calibrate the decode-step cost on the GPU, then run the rollout scans of
+    the rollout-efficiency study through the native engine-model simulator."""
+    import torch
+
+    from paper_2609_36608_amd import binding
+
+    if not torch.cuda.is_available():
+        print("bench.py: no GPU visible", file=sys.stderr)
+        return 1
+    dev = torch.device("cuda", 0)
+    torch.cuda.set_device(dev)
+    cal = calibrate_attention(torch, dev)
+    weight_s = SIM_PARAMS * 2 / (COPY_CEILING_GBS * 1e9)
+    eng = dict(step_base=weight_s + SIM_LAYERS * cal["per_call_s"],
+               step_per_kv_token=SIM_LAYERS * cal["per_kv_token_s"],
+               prefill_per_token=2 * SIM_PARAMS / 680e12)
+    n = 16
+
+    def speedup(turns, b_max, full_tokens):
+        ctx = sim_contexts(n, turns)
+        v = binding.rollout_simulate_engine(binding.ROLLOUT_VANILLA, ctx, 16, full_tokens, b_max, **eng)
+        a = binding.rollout_simulate_engine(binding.ROLLOUT_ACTFIRST, ctx, 16, full_tokens, b_max, **eng)
+        return v["completion"] / a["completion"], v, a
+
+    t0 = time.perf_counter()
+    conc = {ft: {b: round(speedup(30, b, ft)[0], 3) for b in (16, 32, 64, 128, 256)} for ft in (128, 512)}
+    hor = {ft: {t: round(speedup(t, 256, ft)[0], 3) for t in (1, 2, 4, 8, 16, 30)} for ft in (128, 512)}
+    head, v, a = speedup(30, 256, 512)
+    native_s = time.perf_counter() - t0
+    nsim = 2 * (5 + 6) * 2 + 2
+    requests = 2 * n * 30
+    result = {
+        "metric": SIM_METRIC,
+        "value": round(head, 4),
+        "unit": "x",
+        "n_gpus": 1,
+        "steps": 1,
+        "warmup": 0,
+        "ms_per_step": round(native_s / nsim * 1e3, 3),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f64",
+        "data": "synthetic",
+        "config": {
+            "workload": "rollout-efficiency scans: 16 tasks, fixed contexts U{1500..3000} tokens, 16-token fast "
+                        "actions, 128- or 512-token full responses; b_max scan at T=30, T scan at b_max=256",
+            "engine": {k: float(f"{x:.6g}") for k, x in eng.items()},
+            "engine_sources": "step_per_kv_token and the per-layer call cost: ctx_decode_attn_run timed on this GPU "
+                              "at 28 layers, 16/8 heads; step weight streaming: 1.72e9 bf16 parameters at the measured "
+                              "7.09 TB/s read ceiling; prefill: 2 x parameters flops per token at the measured "
+                              "prefill-kernel rate (680 TFLOP/s)",
+            "parallelism": "none (1 GPU)",
+        },
+        "speedup_vs_b_max_T30": conc,
+        "speedup_vs_T_b_max256": hor,
+        "paper_measured_A100_vllm": {"b_max16_to_256_128tok": [0.80, 1.49], "b_max16_to_256_512tok": [0.92, 2.42]},
+        "completion_s": {"vanilla": round(v["completion"], 4), "actfirst": round(a["completion"], 4)},
+        "simulations_per_s": round(nsim / native_s, 2),
+        "requests_per_s": round(nsim * requests / native_s, 1),
+        "roofline": {
+            "bound": "hbm",
+            "achieved": round(cal["achieved_gbs"], 2),
+            "peak": HBM_PEAK_GBS,
+            "unit": "GB/s",
+            "frac": round(cal["achieved_gbs"] / HBM_PEAK_GBS, 4),
+            "traffic": None,
+            "kernel": "ctx_decode_attn_run calls of the calibration (28-layer Qwen3-1.7B shape, batches 16..256)",
+            "bytes_per_launch": round(cal["bytes_per_call"]),
+            "avg_launch_us": round(cal["avg_call_us"], 3),
+        },
+    }
+    if not args.no_cpu_baseline:
+        from oracle import oracle_sched as sch
+
+        ctx = sim_contexts(n, 30).tolist()
+        t1 = time.perf_counter()
+        reps = 0
+        while True:
+            sch.simulate_engine(sch.VANILLA, ctx, 16, 512, 256, eng["step_base"], eng["step_per_kv_token"],
+                                eng["prefill_per_token"])
+            sch.simulate_engine(sch.ACTFIRST, ctx, 16, 512, 256, eng["step_base"], eng["step_per_kv_token"],
+                                eng["prefill_per_token"])
+            reps += 1
+            el = time.perf_counter() - t1
+            if el >= args.cpu_seconds or el / reps * (reps + 1) > 3 * args.cpu_seconds:
+                break
+        result["cpu_baseline"] = {
+            "value": round(2 * reps * requests / el, 1),
+            "unit": "requests/s",
+            "cores": 1,
+            "kind": "oracle",
+            "sample": f"the headline pair of simulations (Vanilla and ActFirst, T=30, b_max=256, 512 tokens), "
+                      f"{reps}x in {el:.1f} s; pure-Python oracle",
+        }
+    print(json.dumps(result), flush=True)
+    return 0
+
+
 def main() -> int:
     ap = argparse.ArgumentParser(description=__doc__)
     ap.add_argument("--gpus", type=int, default=1)
@@ -435,6 +594,8 @@ def main() -> int:
                          "(act_first_burst)")
     ap.add_argument("--opd", action="store_true",
                     help="time the fused OPD token loss + logits gradient instead (64 responses, Qwen3 vocabulary)")
+    ap.add_argument("--sim", action="store_true",
+                    help="calibrate the decode-step cost on the GPU and run the rollout scheduling scans")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--calibrate-copy-gib", type=float, default=0.0,
@@ -454,6 +615,8 @@ def main() -> int:
         return bench_prefill(args)
     if args.opd:
         return bench_opd(args)
+    if args.sim:
+        return bench_sim(args)
 
     import torch
 

@@ -29,6 +29,8 @@ EXPORTS = (
     "ctx_decode_attn_run_paged",
     "ctx_prefill_attn_run",
     "ctx_opd_loss_run",
+    "ctx_rollout_simulate",
+    "ctx_rollout_simulate_engine",
     "ctx_decode_attn_destroy",
     "ctx_decode_attn_status_string",
     "ctx_decode_attn_last_error",
@@ -59,6 +61,21 @@ class OpdParams(ctypes.Structure):
 
     def __init__(self, log_ratio_clip=20.0, clip_delta=0.2, dual_clip=3.0, eps=1e-8):
         super().__init__(log_ratio_clip, clip_delta, dual_clip, eps)
+
+
+class RolloutConfig(ctypes.Structure):
+    _fields_ = [("policy", ctypes.c_int32), ("num_tasks", ctypes.c_int32), ("turns", ctypes.c_int32),
+                ("max_concurrency", ctypes.c_int32)]
+
+
+class RolloutEngine(ctypes.Structure):
+    _fields_ = [("step_base", ctypes.c_double), ("step_per_kv_token", ctypes.c_double),
+                ("prefill_per_token", ctypes.c_double), ("fast_tokens", ctypes.c_int32),
+                ("full_tokens", ctypes.c_int32)]
+
+
+ROLLOUT_VANILLA = 0
+ROLLOUT_ACTFIRST = 1
 
 
 class CtxError(RuntimeError):
@@ -95,6 +112,11 @@ def load_library(path: str | None = None):
     lib.ctx_opd_loss_run.argtypes = [vp, ctypes.c_int64, i32, vp, vp, vp, vp, vp, i32, i32,
                                      ctypes.POINTER(OpdParams), vp, vp, vp, vp, vp, ctypes.c_int64, vp]
     lib.ctx_opd_loss_run.restype = ctypes.c_int
+    lib.ctx_rollout_simulate.argtypes = [ctypes.POINTER(RolloutConfig), vp, vp, vp, vp, vp, vp]
+    lib.ctx_rollout_simulate.restype = ctypes.c_int
+    lib.ctx_rollout_simulate_engine.argtypes = [ctypes.POINTER(RolloutConfig), ctypes.POINTER(RolloutEngine), vp, vp,
+                                                vp, vp, vp, vp]
+    lib.ctx_rollout_simulate_engine.restype = ctypes.c_int
     lib.ctx_decode_attn_destroy.argtypes = [vp]
     lib.ctx_decode_attn_destroy.restype = ctypes.c_int
     lib.ctx_decode_attn_status_string.argtypes = [ctypes.c_int]
@@ -337,3 +359,51 @@ def opd_loss(logits, tokens, old_logp, teacher_logp, mask, seq_starts, params: O
     if rc != CTX_OK:
         raise error_for(lib, rc)
     return res
+
+
+def _rollout_outputs(n, turns):
+    import numpy as np
+
+    return (np.zeros(1, np.float64), np.full(n * turns * 2, -1.0), np.full(n * turns * 2, -1.0),
+            np.zeros(1, np.int32))
+
+
+def rollout_simulate(policy: int, fast_latency, full_latency, max_concurrency: int) -> dict:
+    """Latency model of ctx_rollout_simulate.  fast_latency, full_latency:
+    [N, T] seconds (host arrays).  Returns completion, start and end [N, T, 2]
+    (kind 0 = fast action, 1 = full response; -1 = not submitted) and peak."""
+    import numpy as np
+
+    lib = load_library()
+    full = np.ascontiguousarray(full_latency, dtype=np.float64)
+    fast = np.ascontiguousarray(fast_latency, dtype=np.float64)
+    n, turns = full.shape
+    cfg = RolloutConfig(policy, n, turns, max_concurrency)
+    comp, st, en, pk = _rollout_outputs(n, turns)
+    p = lambda a: a.ctypes.data_as(ctypes.c_void_p)  # noqa: E731
+    rc = lib.ctx_rollout_simulate(ctypes.byref(cfg), p(fast), p(full), p(comp), p(st), p(en), p(pk))
+    if rc != CTX_OK:
+        raise error_for(lib, rc)
+    return {"completion": float(comp[0]), "start": st.reshape(n, turns, 2), "end": en.reshape(n, turns, 2),
+            "peak": int(pk[0])}
+
+
+def rollout_simulate_engine(policy: int, context_tokens, fast_tokens: int, full_tokens: int, max_concurrency: int,
+                            step_base: float, step_per_kv_token: float, prefill_per_token: float) -> dict:
+    """Engine model of ctx_rollout_simulate_engine; context_tokens [N, T]."""
+    import numpy as np
+
+    lib = load_library()
+    ctx = np.ascontiguousarray(context_tokens, dtype=np.int32)
+    n, turns = ctx.shape
+    cfg = RolloutConfig(policy, n, turns, max_concurrency)
+    eng = RolloutEngine(step_base, step_per_kv_token, prefill_per_token, fast_tokens, full_tokens)
+    comp, st, en, pk = _rollout_outputs(n, turns)
+    steps = np.zeros(1, np.int64)
+    p = lambda a: a.ctypes.data_as(ctypes.c_void_p)  # noqa: E731
+    rc = lib.ctx_rollout_simulate_engine(ctypes.byref(cfg), ctypes.byref(eng), p(ctx), p(comp), p(st), p(en),
+                                         p(pk), p(steps))
+    if rc != CTX_OK:
+        raise error_for(lib, rc)
+    return {"completion": float(comp[0]), "start": st.reshape(n, turns, 2), "end": en.reshape(n, turns, 2),
+            "peak": int(pk[0]), "steps": int(steps[0])}
