@@ -864,7 +864,10 @@ __global__ __launch_bounds__(64 * kPrefillWaves) void prefill_kernel(
           plo[ct][j] = lw;
         }
       }
-      // O^T += V^T P^T: the K dimension holds tokens 4c..4c+3 of both halves
+      // O^T += V^T P^T: the K dimension holds tokens 4c..4c+3 of both halves.
+      // The MFMA stream runs at raised wave priority, so that the other wave
+      // on this SIMD fills the matrix core's issue gaps with its softmax.
+      __builtin_amdgcn_s_setprio(1);
 #pragma unroll
       for (int nb = 0; nb < 8; ++nb) {
         const int off = v_row + (((2 * nb + v_ch) ^ v_swz) << 3);
@@ -878,6 +881,7 @@ __global__ __launch_bounds__(64 * kPrefillWaves) void prefill_kernel(
         for (int ct = 0; ct < kPrefillTiles; ++ct)
           o[ct][nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(va, as_bf16x8(plo[ct]), o[ct][nb], 0, 0, 0);
       }
+      __builtin_amdgcn_s_setprio(0);
     }
     if (more) {  // the other buffer was released at the previous barrier
 #pragma unroll

@@ -150,3 +150,13 @@ def test_prefill_abi():
         assert lib.ctx_prefill_attn_run(h, P(z), P(kv), P(kv), P(i), P(i), P(i), None, 2, 1, 0.1, P(o), None) == bd.CTX_ERR_INVALID_ARG
         assert lib.ctx_prefill_attn_run(h, P(z), P(kv), P(kv), P(i), P(i), P(i), P(i), 2, -1, 0.1, P(o), None) == bd.CTX_ERR_INVALID_ARG
         torch.cuda.synchronize()
+
+
+def test_prefill_bf16_output():
+    """bf16 output is the round-to-nearest-even of the fp32 result."""
+    w, lay, lens, nq, qs, q, k, v = prefill_case(31, 32, 8, batch=5, hist=(0, 300), new=(1, 100))
+    f32 = run_prefill(w, lay, lens, nq, qs, q, k, v, out_dtype=torch.float32)
+    b16 = run_prefill(w, lay, lens, nq, qs, q, k, v, out_dtype=torch.bfloat16)
+    rows = np.concatenate([np.arange(qs[b], qs[b] + nq[b]) for b in range(5)])
+    want = wl.bf16_bits_to_f32(wl.f32_to_bf16_bits(f32[rows].astype(np.float32)))
+    np.testing.assert_array_equal(b16[rows], want)
