@@ -22,13 +22,14 @@ def rand_bits(rng, shape):
     return bf(rng.standard_normal(shape).astype(np.float32))
 
 
-def run_paged(w, q, kp, vp, bt, lens, page_tokens, split=0, k_new=None, v_new=None, max_seq_len=None):
+def run_paged(w, q, kp, vp, bt, lens, page_tokens, split=0, k_new=None, v_new=None, max_seq_len=None,
+              out_dtype=torch.float32):
     """Returns (out, k_pages after, v_pages after) as host arrays."""
     b = len(lens)
     kpd, vpd = up_bf16(kp), up_bf16(vp)
     with DecodeAttention(w.num_q_heads, w.num_kv_heads, b, max_seq_len or int(np.max(lens)),
-                         split_tokens=split, page_tokens=page_tokens) as attn:
-        buf = torch.full((b + 1, w.num_q_heads, 128), -777.0, dtype=torch.float32, device=dev())
+                         split_tokens=split, page_tokens=page_tokens, out_dtype=out_dtype) as attn:
+        buf = torch.full((b + 1, w.num_q_heads, 128), -777.0, dtype=out_dtype, device=dev())
         out = buf[:b]
         attn.run_paged(up_bf16(q), kpd, vpd, up_i32(bt), up_i32(lens), w.scale, out,
                        k_new=None if k_new is None else up_bf16(k_new),
@@ -36,7 +37,7 @@ def run_paged(w, q, kp, vp, bt, lens, page_tokens, split=0, k_new=None, v_new=No
         torch.cuda.synchronize()
         assert (buf[b] == -777.0).all(), "write past the end of out"
     as_bits = lambda t: t.view(torch.int16).cpu().numpy().view(np.uint16)  # noqa: E731
-    return out.cpu().numpy(), as_bits(kpd), as_bits(vpd)
+    return out.float().cpu().numpy(), as_bits(kpd), as_bits(vpd)
 
 
 def paged_case(seed, page_tokens, batch=20, hq=32, hkv=8, lo=1, hi=900, steps=4):
@@ -177,3 +178,22 @@ def test_paged_abi_errors():
     for kw in (dict(page_tokens=24), dict(page_tokens=16, split_tokens=24), dict(page_tokens=-16)):
         with pytest.raises(CtxError):
             DecodeAttention(16, 8, 2, 32, **kw)
+
+
+def test_paged_bf16_output_and_many_sequences():
+    """bf16 output equals the rounded fp32 output, and a batch of more than
+    64 sequences (the range search over the whole batch) with an append."""
+    w, lay, q, kp, vp, bt, rng = paged_case(31, 16, batch=150, hi=400)
+    f32, _, _ = run_paged(w, q, kp, vp, bt, lay.lens, 16, split=0, max_seq_len=lay.max_seq_len)
+    b16, _, _ = run_paged(w, q, kp, vp, bt, lay.lens, 16, split=0, max_seq_len=lay.max_seq_len,
+                          out_dtype=torch.bfloat16)
+    np.testing.assert_array_equal(b16, wl.bf16_bits_to_f32(wl.f32_to_bf16_bits(f32.astype(np.float32))))
+    ref = oracle.decode_attn_paged(q, kp, vp, bt, lay.lens, w.scale)
+    assert_parity(f32, ref, "paged, 150 sequences")
+    k_new = rand_bits(rng, (w.batch, w.num_kv_heads, 128))
+    v_new = rand_bits(rng, (w.batch, w.num_kv_heads, 128))
+    ref = oracle.decode_attn_paged(q, kp, vp, bt, lay.lens, w.scale, k_new, v_new)
+    for split in (0, 32):
+        got, _, _ = run_paged(w, q, kp, vp, bt, lay.lens, 16, split=split, k_new=k_new, v_new=v_new,
+                              max_seq_len=lay.max_seq_len)
+        assert_parity(got, ref, f"paged append, 150 sequences, split={split}")
