@@ -124,17 +124,6 @@ __global__ __launch_bounds__(256) void opd_weight_kernel(const uint8_t* __restri
   for (int j = s0 + (int)threadIdx.x; j < s1; j += 256) weight[j] = mask[j] ? w : 0.f;
 }
 
-// Store chunk q of a gradient row: whole if it lies below vocab, else only
-// its columns below vocab.
-__device__ __forceinline__ void store_chunk(uint16_t* grow, int q, u32x4 o, int vocab) {
-  if ((q + 1) * kChunk <= vocab) {
-    __builtin_nontemporal_store(o, reinterpret_cast<u32x4*>(grow) + q);
-  } else {
-    for (int e = 0; e < kChunk && q * kChunk + e < vocab; ++e)
-      grow[q * kChunk + e] = (uint16_t)(e & 1 ? o[e >> 1] >> 16 : o[e >> 1] & 0xffffu);
-  }
-}
-
 // eq:opd-dual-clip for one token: the loss and d loss / d rho
 __device__ __forceinline__ void dual_clip_loss(float rho, float a, const OpdParams& p, float* loss,
                                                float* dloss) {

@@ -1,0 +1,376 @@
+// ctx_prefill_attn.hip -- causal prefill attention for gfx950 (MI355X),
+// behind ctx_prefill_attn_run in the C ABI declared in include/ctx_decode_attn.h.
+//
+// Causal prefill of each sequence's newest tokens (the reference next
+// observation the fast action conditions on) against its cache, which already
+// holds their K/V rows.  Query column n of a 16-column MFMA tile is query
+// position n / g, head n % g of one KV group (g divides 16), so every column
+// carries work.  A workgroup of kPrefillWaves waves covers kPrefillCols
+// columns of one (sequence, KV head) and streams 32-token K/V blocks, up to
+// its last query position, through a double-buffered LDS tile that all its
+// waves share.  Per 16 tokens and 16 columns a wave computes
+//   S^T = K Q^T                 (4 MFMA 16x16x32, K rows straight from LDS)
+//   causal mask, lazy online softmax, P = P_hi + P_lo (two bf16 terms)
+//   O^T += V^T [P_hi | P_lo]^T  (8 MFMA 16x16x32: the hi and lo terms are the
+//                                two halves of the K dimension, V^T repeated)
+// where the V^T operand comes from the row-major LDS tile through the LDS
+// transpose read, whose 4 values per lane are tokens 4c..4c+3 of one
+// dimension -- the rows the S^T tile gives each lane.
+
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdint>
+
+#include "ctx_attn_common.h"
+
+namespace {
+
+// Cached variant for data that several workgroups re-read (prefill tiles).
+#ifndef CTX_PREFILL_AUX
+#define CTX_PREFILL_AUX 0
+#endif
+__device__ __forceinline__ u32x4 buf_load16_shared(__amdgpu_buffer_rsrc_t r, int voff, int soff) {
+  return __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, CTX_PREFILL_AUX));
+}
+
+#ifndef CTX_PREFILL_WAVES
+#define CTX_PREFILL_WAVES 4
+#endif
+constexpr int kPrefillWaves = CTX_PREFILL_WAVES;
+#ifndef CTX_PREFILL_TILES
+#define CTX_PREFILL_TILES 3
+#endif
+constexpr int kPrefillTiles = CTX_PREFILL_TILES;  // 16-column tiles per wave
+constexpr int kPrefillCols = kPrefillWaves * kPrefillTiles * 16;
+constexpr int kPrefillBlock = 32;  // tokens per LDS stage
+// 16-byte chunks each thread stages per K (and per V) block
+constexpr int kPrefillLoads = kPrefillBlock * 16 / (64 * kPrefillWaves);
+static_assert(kPrefillLoads >= 1 && kPrefillLoads * 64 * kPrefillWaves == kPrefillBlock * 16,
+              "the workgroup must tile a block's chunks exactly");
+#ifndef CTX_PREFILL_XCD
+#define CTX_PREFILL_XCD 1
+#endif
+
+struct PrefillPlan {
+  int32_t hq;
+  int32_t hkv;
+  int32_t group;
+  int32_t tiles;  // workgroups per (sequence, KV head)
+  int32_t units;  // sequences x KV heads
+  float scale_log2;
+};
+
+typedef short s16x8 __attribute__((ext_vector_type(8)));
+
+// LDS tile of K or V: token row t holds its 16 chunks of 8 dimensions with
+// chunk ch at slot ch ^ prefill_swizzle(t): conflict-free for the staging
+// writes, the K operand reads (16 tokens x one chunk) and the transpose reads
+// (4 tokens x 4 dimensions per 16 lanes).
+__device__ __forceinline__ int prefill_swizzle(int t) { return ((t & 7) << 1) | ((t >> 3) & 1); }
+
+// LDS transpose read: in each 16-lane group, lane l receives element l % 4 of
+// the 8-byte rows addressed by lanes l / 4, 4 + l / 4, 8 + l / 4, 12 + l / 4.
+__device__ __forceinline__ s16x4 lds_read_tr16(const uint16_t* p) {
+  typedef s16x4 __attribute__((address_space(3))) * lds_s16x4;
+  return __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4)(p));
+}
+
+// Split a pair of non-negative floats into bf16 hi = the value with its low 16
+// bits cleared and bf16 lo = round-to-nearest-even of the exact remainder, so
+// that hi + lo carries 16 significant bits; both packed as (a, b).
+__device__ __forceinline__ void split_bf16x2(float a, float b, uint32_t* hi, uint32_t* lo) {
+  const uint32_t ua = __float_as_uint(a), ub = __float_as_uint(b);
+  *hi = __builtin_amdgcn_perm(ub, ua, 0x07060302u);  // high halves of a and b
+  *lo = pack_bf16x2(a - __uint_as_float(ua & 0xffff0000u), b - __uint_as_float(ub & 0xffff0000u));
+}
+
+template <typename OutT>
+__global__ __launch_bounds__(64 * kPrefillWaves) void prefill_kernel(
+    const uint16_t* __restrict__ q, const uint16_t* __restrict__ kc, const uint16_t* __restrict__ vc,
+    const int32_t* __restrict__ offs, const int32_t* __restrict__ lens,
+    const int32_t* __restrict__ q_starts, const int32_t* __restrict__ q_lens, PrefillPlan pp,
+    OutT* __restrict__ out) {
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int n = lane & 15;
+  const int c = lane >> 4;
+  const int g = pp.group;
+#if CTX_PREFILL_XCD
+  // consecutive workgroups go to different XCDs; keep every tile of a unit on
+  // one XCD so that its L2 serves the tiles' re-reads of the unit's K/V
+  const int slot = blockIdx.x / kXcds;
+  const int tile = slot % pp.tiles;
+  const int unit = (slot / pp.tiles) * kXcds + (int)(blockIdx.x % kXcds);
+  if (unit >= pp.units) return;
+#else
+  const int tile = blockIdx.x % pp.tiles;
+  const int unit = blockIdx.x / pp.tiles;
+#endif
+  const int kv = unit % pp.hkv;
+  const int b = unit / pp.hkv;
+  const int nq = q_lens[b];
+  const int first_q = tile * (kPrefillCols / g);
+  if (first_q >= nq) return;  // the whole workgroup: nothing to do
+  const int seq_len = lens[b];
+  const int hist = seq_len - nq;  // position of query 0
+  const int last_q = (first_q + kPrefillCols / g < nq ? first_q + kPrefillCols / g : nq) - 1;
+  const int kv_end = hist + last_q + 1;  // tokens any query of the workgroup attends to
+  const size_t row_elems = (size_t)pp.hkv * kHeadDim;
+  const int row_bytes = (int)(row_elems * 2);
+  const uint16_t* kseq = kc + (size_t)offs[b] * row_elems + (size_t)kv * kHeadDim;
+  const uint16_t* vseq = vc + (size_t)offs[b] * row_elems + (size_t)kv * kHeadDim;
+
+  __shared__ __attribute__((aligned(16))) uint16_t lds_k[2][kPrefillBlock * kHeadDim];
+  __shared__ __attribute__((aligned(16))) uint16_t lds_v[2][kPrefillBlock * kHeadDim];
+
+  // logits in log2 units are s * cs with cs >= 0: a negative scale flips the
+  // sign of q instead (exact in bf16), so that max(s) * cs = max(s * cs)
+  const float cs = fabsf(pp.scale_log2);
+  const uint32_t qflip = pp.scale_log2 < 0.f ? 0x80008000u : 0u;
+
+  // this lane's query column in each tile: query index qi, head kv * g + hh,
+  // attending to positions 0 .. last_pos (columns past the last query attend
+  // to the whole block range and are not written)
+  int qi[kPrefillTiles], hh[kPrefillTiles], last_pos[kPrefillTiles];
+  bf16x8 qb[kPrefillTiles][4];
+#pragma unroll
+  for (int ct = 0; ct < kPrefillTiles; ++ct) {
+    const int col = tile * kPrefillCols + (wave * kPrefillTiles + ct) * 16 + n;
+    qi[ct] = col / g;
+    hh[ct] = col - qi[ct] * g;
+    const bool valid = qi[ct] < nq;
+    last_pos[ct] = valid ? hist + qi[ct] : kv_end - 1;
+    if (valid) {
+      const uint16_t* qrow =
+          q + ((size_t)(q_starts[b] + qi[ct]) * pp.hq + (size_t)kv * g + hh[ct]) * kHeadDim + 8 * c;
+#pragma unroll
+      for (int kk = 0; kk < 4; ++kk) qb[ct][kk] = as_bf16x8(load16(qrow + 32 * kk) ^ qflip);
+    } else {
+#pragma unroll
+      for (int kk = 0; kk < 4; ++kk) qb[ct][kk] = as_bf16x8(u32x4{0u, 0u, 0u, 0u});
+    }
+  }
+  // the wave's query positions: tokens at or below mask_from are seen by every
+  // column; tokens from wave_end on by none (a wave past the last query idles)
+  const int wave_q0 = (tile * kPrefillCols + wave * kPrefillTiles * 16) / g;
+  const int wave_q1 = (tile * kPrefillCols + (wave + 1) * kPrefillTiles * 16 - 1) / g;
+  const bool wave_active = wave_q0 < nq;
+  const int mask_from = hist + wave_q0;
+  const int wave_end = hist + (wave_q1 < last_q ? wave_q1 : last_q) + 1;
+
+  Softmax st[kPrefillTiles];
+  f32x4 o[kPrefillTiles][8];
+#pragma unroll
+  for (int ct = 0; ct < kPrefillTiles; ++ct) {
+    st[ct] = Softmax{-INFINITY, 0.f};
+#pragma unroll
+    for (int nb = 0; nb < 8; ++nb) o[ct][nb] = f32x4{0.f, 0.f, 0.f, 0.f};
+  }
+
+  // cooperative block loads: thread tid fetches chunk tid % 16 of tokens
+  // tid / 16 + r * (4 * kPrefillWaves), r < kPrefillLoads, of K and of V; past
+  // kv_end the buffer bound returns zeros
+  int ld_slot[kPrefillLoads], voff[kPrefillLoads];
+#pragma unroll
+  for (int r = 0; r < kPrefillLoads; ++r) {
+    const int t = (tid >> 4) + r * 4 * kPrefillWaves;
+    ld_slot[r] = t * kHeadDim + (((tid & 15) ^ prefill_swizzle(t)) << 3);
+    voff[r] = t * row_bytes + (tid & 15) * 16;
+  }
+  u32x4 pk[kPrefillLoads], pv[kPrefillLoads];
+  {
+    const uint32_t bytes = (uint32_t)((kv_end < kPrefillBlock ? kv_end : kPrefillBlock) * row_bytes);
+    const __amdgpu_buffer_rsrc_t rk = make_rsrc(kseq, bytes);
+    const __amdgpu_buffer_rsrc_t rv = make_rsrc(vseq, bytes);
+#pragma unroll
+    for (int r = 0; r < kPrefillLoads; ++r) {
+      pk[r] = buf_load16_shared(rk, voff[r], 0);
+      pv[r] = buf_load16_shared(rv, voff[r], 0);
+    }
+#pragma unroll
+    for (int r = 0; r < kPrefillLoads; ++r) {
+      *reinterpret_cast<u32x4*>(&lds_k[0][ld_slot[r]]) = pk[r];
+      *reinterpret_cast<u32x4*>(&lds_v[0][ld_slot[r]]) = pv[r];
+    }
+  }
+  __syncthreads();
+
+  // per-lane LDS offsets of the operand reads within a 16-token half block
+  int k_off[4];
+#pragma unroll
+  for (int kk = 0; kk < 4; ++kk) k_off[kk] = n * kHeadDim + (((4 * kk + c) ^ prefill_swizzle(n)) << 3);
+  const int v_tok = 4 * c + (n >> 2);
+  const int v_row = v_tok * kHeadDim + 4 * (n & 1);
+  const int v_swz = prefill_swizzle(v_tok);
+  const int v_ch = (n & 3) >> 1;
+
+  int buf = 0;
+  for (int t0 = 0; t0 < kv_end; t0 += kPrefillBlock) {
+    const bool more = t0 + kPrefillBlock < kv_end;
+    if (more) {  // next block in flight during this one's math
+      const int rem = kv_end - t0 - kPrefillBlock;
+      const uint32_t bytes = (uint32_t)((rem < kPrefillBlock ? rem : kPrefillBlock) * row_bytes);
+      const __amdgpu_buffer_rsrc_t rk = make_rsrc(kseq + (size_t)(t0 + kPrefillBlock) * row_elems, bytes);
+      const __amdgpu_buffer_rsrc_t rv = make_rsrc(vseq + (size_t)(t0 + kPrefillBlock) * row_elems, bytes);
+#pragma unroll
+      for (int r = 0; r < kPrefillLoads; ++r) {
+        pk[r] = buf_load16_shared(rk, voff[r], 0);
+        pv[r] = buf_load16_shared(rv, voff[r], 0);
+      }
+    }
+    if (wave_active && t0 < wave_end) {
+      const uint16_t* kt = lds_k[buf];
+      const uint16_t* vt = lds_v[buf];
+      // S^T of tokens t0 + 16 h + 4c + i (i < 4) for every column tile
+      f32x4 sc[kPrefillTiles][2];
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        u32x4 kr[4];
+#pragma unroll
+        for (int kk = 0; kk < 4; ++kk)
+          kr[kk] = *reinterpret_cast<const u32x4*>(kt + 16 * h * kHeadDim + k_off[kk]);
+#pragma unroll
+        for (int ct = 0; ct < kPrefillTiles; ++ct) sc[ct][h] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int kk = 0; kk < 4; ++kk)
+#pragma unroll
+          for (int ct = 0; ct < kPrefillTiles; ++ct)
+            sc[ct][h] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(kr[kk]), qb[ct][kk], sc[ct][h], 0, 0, 0);
+      }
+      const bool masked = t0 + kPrefillBlock - 1 > mask_from;
+      u32x4 phi[kPrefillTiles], plo[kPrefillTiles];
+#pragma unroll
+      for (int ct = 0; ct < kPrefillTiles; ++ct) {
+        float x[8];
+        float lmax;
+        if (masked) {  // blocks on the causal diagonal (or past kv_end)
+#pragma unroll
+          for (int h = 0; h < 2; ++h)
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+              x[4 * h + i] = (t0 + 16 * h + 4 * c + i > last_pos[ct]) ? -INFINITY : sc[ct][h][i] * cs;
+          lmax = fmaxf(fmaxf(fmaxf(x[0], x[1]), fmaxf(x[2], x[3])), fmaxf(fmaxf(x[4], x[5]), fmaxf(x[6], x[7])));
+        } else {
+          const f32x4 a = sc[ct][0], e = sc[ct][1];
+          lmax = fmaxf(fmaxf(fmaxf(a[0], a[1]), fmaxf(a[2], a[3])), fmaxf(fmaxf(e[0], e[1]), fmaxf(e[2], e[3]))) * cs;
+        }
+        // lazy rescale: only when some logit exceeds the running max by 2^8;
+        // the column max (across the 4 lanes of a column) only then
+        if (__any(lmax > st[ct].m + kLazyRescale)) {
+          float mx = fmaxf(lmax, __shfl_xor(lmax, 16));
+          mx = fmaxf(mx, __shfl_xor(mx, 32));
+          const float m_new = fmaxf(st[ct].m, mx);
+          const float alpha = fast_exp2(st[ct].m - m_new);
+          st[ct].l *= alpha;
+#pragma unroll
+          for (int nb = 0; nb < 8; ++nb) o[ct][nb] *= alpha;
+          st[ct].m = m_new;
+        }
+        float pr[8];
+        if (masked) {
+#pragma unroll
+          for (int i = 0; i < 8; ++i) pr[i] = fast_exp2(x[i] - st[ct].m);
+        } else {
+#pragma unroll
+          for (int h = 0; h < 2; ++h)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) pr[4 * h + i] = fast_exp2(fmaf(sc[ct][h][i], cs, -st[ct].m));
+        }
+        st[ct].l += ((pr[0] + pr[1]) + (pr[2] + pr[3])) + ((pr[4] + pr[5]) + (pr[6] + pr[7]));
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          uint32_t hw, lw;
+          split_bf16x2(pr[2 * j], pr[2 * j + 1], &hw, &lw);
+          phi[ct][j] = hw;
+          plo[ct][j] = lw;
+        }
+      }
+      // O^T += V^T P^T: the K dimension holds tokens 4c..4c+3 of both halves.
+      // The MFMA stream runs at raised wave priority, so that the other wave
+      // on this SIMD fills the matrix core's issue gaps with its softmax.
+      __builtin_amdgcn_s_setprio(1);
+#pragma unroll
+      for (int nb = 0; nb < 8; ++nb) {
+        const int off = v_row + (((2 * nb + v_ch) ^ v_swz) << 3);
+        const s16x4 v0 = lds_read_tr16(vt + off);
+        const s16x4 v1 = lds_read_tr16(vt + 16 * kHeadDim + off);
+        const bf16x8 va = __builtin_bit_cast(bf16x8, __builtin_shufflevector(v0, v1, 0, 1, 2, 3, 4, 5, 6, 7));
+#pragma unroll
+        for (int ct = 0; ct < kPrefillTiles; ++ct)
+          o[ct][nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(va, as_bf16x8(phi[ct]), o[ct][nb], 0, 0, 0);
+#pragma unroll
+        for (int ct = 0; ct < kPrefillTiles; ++ct)
+          o[ct][nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(va, as_bf16x8(plo[ct]), o[ct][nb], 0, 0, 0);
+      }
+      __builtin_amdgcn_s_setprio(0);
+    }
+    if (more) {  // the other buffer was released at the previous barrier
+#pragma unroll
+      for (int r = 0; r < kPrefillLoads; ++r) {
+        *reinterpret_cast<u32x4*>(&lds_k[buf ^ 1][ld_slot[r]]) = pk[r];
+        *reinterpret_cast<u32x4*>(&lds_v[buf ^ 1][ld_slot[r]]) = pv[r];
+      }
+    }
+    __syncthreads();
+    buf ^= 1;
+  }
+
+#pragma unroll
+  for (int ct = 0; ct < kPrefillTiles; ++ct) {
+    float l_tot = st[ct].l + __shfl_xor(st[ct].l, 16);
+    l_tot += __shfl_xor(l_tot, 32);
+    if (qi[ct] < nq) {
+      const float inv = 1.0f / l_tot;
+      OutT* orow = out + ((size_t)(q_starts[b] + qi[ct]) * pp.hq + (size_t)kv * g + hh[ct]) * kHeadDim + 4 * c;
+#pragma unroll
+      for (int nb = 0; nb < 8; ++nb) store4<OutT>(orow + 16 * nb, o[ct][nb] * inv);
+    }
+  }
+}
+
+}  // namespace
+
+extern "C" int ctx_prefill_attn_run(ctx_decode_attn* h, const void* q, const void* k_cache, const void* v_cache,
+                         const int32_t* seq_offsets, const int32_t* seq_lens, const int32_t* q_starts,
+                         const int32_t* q_lens, int32_t num_seqs, int32_t max_q_len, float scale,
+                         void* out, void* stream) {
+  int rc = check_common(h, num_seqs, scale);
+  if (rc != CTX_OK) return rc;
+  const ctx_decode_attn_desc& d = h->desc;
+  const int g = d.num_q_heads / d.num_kv_heads;
+  if (16 % g != 0)
+    return fail(CTX_ERR_UNSUPPORTED, "prefill needs a group size dividing 16 (got %d)", g);
+  if (max_q_len < 0) return fail(CTX_ERR_INVALID_ARG, "max_q_len %d < 0", max_q_len);
+  if (num_seqs == 0 || max_q_len == 0) return CTX_OK;
+  if (q == nullptr || k_cache == nullptr || v_cache == nullptr || seq_offsets == nullptr ||
+      seq_lens == nullptr || q_starts == nullptr || q_lens == nullptr || out == nullptr)
+    return fail(CTX_ERR_INVALID_ARG, "NULL data pointer");
+  if (!aligned16(q) || !aligned16(k_cache) || !aligned16(v_cache) || !aligned16(out))
+    return fail(CTX_ERR_ALIGNMENT, "q, k_cache, v_cache and out must be 16-byte aligned");
+  rc = check_device(h);
+  if (rc != CTX_OK) return rc;
+  PrefillPlan pp;
+  pp.hq = d.num_q_heads;
+  pp.hkv = d.num_kv_heads;
+  pp.group = g;
+  pp.tiles = (int32_t)(((int64_t)max_q_len * g + kPrefillCols - 1) / kPrefillCols);
+  pp.scale_log2 = (float)((double)scale * 1.4426950408889634);
+  pp.units = num_seqs * d.num_kv_heads;
+  const int64_t blocks = (CTX_PREFILL_XCD ? round_up(pp.units, kXcds) : (int64_t)pp.units) * pp.tiles;
+  if (blocks > INT32_MAX) return fail(CTX_ERR_INVALID_ARG, "prefill grid too large");
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  const uint16_t* qp = static_cast<const uint16_t*>(q);
+  const uint16_t* kp = static_cast<const uint16_t*>(k_cache);
+  const uint16_t* vp = static_cast<const uint16_t*>(v_cache);
+  if (d.out_dtype == CTX_DTYPE_F32)
+    hipLaunchKernelGGL(prefill_kernel<float>, dim3((unsigned)blocks), dim3(64 * kPrefillWaves), 0, s, qp,
+                       kp, vp, seq_offsets, seq_lens, q_starts, q_lens, pp, static_cast<float*>(out));
+  else
+    hipLaunchKernelGGL(prefill_kernel<uint16_t>, dim3((unsigned)blocks), dim3(64 * kPrefillWaves), 0, s,
+                       qp, kp, vp, seq_offsets, seq_lens, q_starts, q_lens, pp, static_cast<uint16_t*>(out));
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return hip_fail(e, "kernel launch");
+  return CTX_OK;
+}
