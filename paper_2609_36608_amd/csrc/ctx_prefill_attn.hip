@@ -8,7 +8,8 @@
 // carries work.  A workgroup of kPrefillWaves waves covers kPrefillCols
 // columns of one (sequence, KV head) and streams 32-token K/V blocks, up to
 // its last query position, through a double-buffered LDS tile that all its
-// waves share.  Per 16 tokens and 16 columns a wave computes
+// waves share; the blocks are loaded straight into LDS, the next one during
+// the current one's math.  Per 16 tokens and 16 columns a wave computes
 //   S^T = K Q^T                 (4 MFMA 16x16x32, K rows straight from LDS)
 //   causal mask, lazy online softmax, P = P_hi + P_lo (two bf16 terms)
 //   O^T += V^T [P_hi | P_lo]^T  (8 MFMA 16x16x32: the hi and lo terms are the
@@ -34,6 +35,8 @@ __device__ __forceinline__ u32x4 buf_load16_shared(__amdgpu_buffer_rsrc_t r, int
   return __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, CTX_PREFILL_AUX));
 }
 
+constexpr int kWaitVmcnt0 = 0x0F70;  // s_waitcnt vmcnt(0), expcnt and lgkmcnt left open
+typedef __attribute__((address_space(3))) void lds_void;
 #ifndef CTX_PREFILL_WAVES
 #define CTX_PREFILL_WAVES 4
 #endif
@@ -122,8 +125,10 @@ __global__ __launch_bounds__(64 * kPrefillWaves) void prefill_kernel(
   const uint16_t* kseq = kc + (size_t)offs[b] * row_elems + (size_t)kv * kHeadDim;
   const uint16_t* vseq = vc + (size_t)offs[b] * row_elems + (size_t)kv * kHeadDim;
 
-  __shared__ __attribute__((aligned(16))) uint16_t lds_k[2][kPrefillBlock * kHeadDim];
-  __shared__ __attribute__((aligned(16))) uint16_t lds_v[2][kPrefillBlock * kHeadDim];
+  __shared__ __attribute__((aligned(16))) uint16_t lds_k0[kPrefillBlock * kHeadDim];
+  __shared__ __attribute__((aligned(16))) uint16_t lds_v0[kPrefillBlock * kHeadDim];
+  __shared__ __attribute__((aligned(16))) uint16_t lds_k1[kPrefillBlock * kHeadDim];
+  __shared__ __attribute__((aligned(16))) uint16_t lds_v1[kPrefillBlock * kHeadDim];
 
   // logits in log2 units are s * cs with cs >= 0: a negative scale flips the
   // sign of q instead (exact in bf16), so that max(s) * cs = max(s * cs)
@@ -169,33 +174,30 @@ __global__ __launch_bounds__(64 * kPrefillWaves) void prefill_kernel(
     for (int nb = 0; nb < 8; ++nb) o[ct][nb] = f32x4{0.f, 0.f, 0.f, 0.f};
   }
 
-  // cooperative block loads: thread tid fetches chunk tid % 16 of tokens
-  // tid / 16 + r * (4 * kPrefillWaves), r < kPrefillLoads, of K and of V; past
-  // kv_end the buffer bound returns zeros
-  int ld_slot[kPrefillLoads], voff[kPrefillLoads];
+  // Block loads go straight from memory into the LDS tile (buffer loads with
+  // the LDS flag, no registers held).  Such a load writes lane L's 16 bytes at
+  // LDS base + 16 L: wave w's round r fills slots 0..15 of tokens
+  // 16 r + 4 w + L / 16, so each lane fetches the chunk that the swizzle puts
+  // at its slot.  Past kv_end the buffer bound writes zeros.
+  int dvo[kPrefillLoads];
 #pragma unroll
   for (int r = 0; r < kPrefillLoads; ++r) {
     const int t = (tid >> 4) + r * 4 * kPrefillWaves;
-    ld_slot[r] = t * kHeadDim + (((tid & 15) ^ prefill_swizzle(t)) << 3);
-    voff[r] = t * row_bytes + (tid & 15) * 16;
+    dvo[r] = t * row_bytes + (((tid & 15) ^ prefill_swizzle(t)) << 4);
   }
-  u32x4 pk[kPrefillLoads], pv[kPrefillLoads];
-  {
-    const uint32_t bytes = (uint32_t)((kv_end < kPrefillBlock ? kv_end : kPrefillBlock) * row_bytes);
-    const __amdgpu_buffer_rsrc_t rk = make_rsrc(kseq, bytes);
-    const __amdgpu_buffer_rsrc_t rv = make_rsrc(vseq, bytes);
+  auto issue = [&](int tb, uint16_t* dk, uint16_t* dv) {
+    const int rem = kv_end - tb;
+    const uint32_t bytes = (uint32_t)((rem < kPrefillBlock ? rem : kPrefillBlock) * row_bytes);
+    const __amdgpu_buffer_rsrc_t rk = make_rsrc(kseq + (size_t)tb * row_elems, bytes);
+    const __amdgpu_buffer_rsrc_t rv = make_rsrc(vseq + (size_t)tb * row_elems, bytes);
 #pragma unroll
     for (int r = 0; r < kPrefillLoads; ++r) {
-      pk[r] = buf_load16_shared(rk, voff[r], 0);
-      pv[r] = buf_load16_shared(rv, voff[r], 0);
+      const int row0 = r * 4 * kPrefillWaves + 4 * wave;  // first token row of this wave's round
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rk, (lds_void*)&dk[row0 * kHeadDim], 16, dvo[r], 0, 0, CTX_PREFILL_AUX);
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rv, (lds_void*)&dv[row0 * kHeadDim], 16, dvo[r], 0, 0, CTX_PREFILL_AUX);
     }
-#pragma unroll
-    for (int r = 0; r < kPrefillLoads; ++r) {
-      *reinterpret_cast<u32x4*>(&lds_k[0][ld_slot[r]]) = pk[r];
-      *reinterpret_cast<u32x4*>(&lds_v[0][ld_slot[r]]) = pv[r];
-    }
-  }
-  __syncthreads();
+  };
+  issue(0, lds_k0, lds_v0);
 
   // per-lane LDS offsets of the operand reads within a 16-token half block
   int k_off[4];
@@ -206,23 +208,16 @@ __global__ __launch_bounds__(64 * kPrefillWaves) void prefill_kernel(
   const int v_swz = prefill_swizzle(v_tok);
   const int v_ch = (n & 3) >> 1;
 
-  int buf = 0;
-  for (int t0 = 0; t0 < kv_end; t0 += kPrefillBlock) {
-    const bool more = t0 + kPrefillBlock < kv_end;
-    if (more) {  // next block in flight during this one's math
-      const int rem = kv_end - t0 - kPrefillBlock;
-      const uint32_t bytes = (uint32_t)((rem < kPrefillBlock ? rem : kPrefillBlock) * row_bytes);
-      const __amdgpu_buffer_rsrc_t rk = make_rsrc(kseq + (size_t)(t0 + kPrefillBlock) * row_elems, bytes);
-      const __amdgpu_buffer_rsrc_t rv = make_rsrc(vseq + (size_t)(t0 + kPrefillBlock) * row_elems, bytes);
-#pragma unroll
-      for (int r = 0; r < kPrefillLoads; ++r) {
-        pk[r] = buf_load16_shared(rk, voff[r], 0);
-        pv[r] = buf_load16_shared(rv, voff[r], 0);
-      }
-    }
+  // One 32-token block: wait for this wave's loads of it, then the barrier
+  // (every wave's loads have landed, and every wave is done with the other
+  // stage); the next block's loads go into that stage during this block's
+  // math.  The two stages are distinct LDS arrays named at compile time, so
+  // the compiler's wait before the reads covers only this stage's loads.
+  auto step = [&](int t0, const uint16_t* kt, const uint16_t* vt, uint16_t* nk, uint16_t* nv) {
+    __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
+    __syncthreads();
+    if (t0 + kPrefillBlock < kv_end) issue(t0 + kPrefillBlock, nk, nv);
     if (wave_active && t0 < wave_end) {
-      const uint16_t* kt = lds_k[buf];
-      const uint16_t* vt = lds_v[buf];
       // S^T of tokens t0 + 16 h + 4c + i (i < 4) for every column tile
       f32x4 sc[kPrefillTiles][2];
 #pragma unroll
@@ -306,15 +301,10 @@ __global__ __launch_bounds__(64 * kPrefillWaves) void prefill_kernel(
       }
       __builtin_amdgcn_s_setprio(0);
     }
-    if (more) {  // the other buffer was released at the previous barrier
-#pragma unroll
-      for (int r = 0; r < kPrefillLoads; ++r) {
-        *reinterpret_cast<u32x4*>(&lds_k[buf ^ 1][ld_slot[r]]) = pk[r];
-        *reinterpret_cast<u32x4*>(&lds_v[buf ^ 1][ld_slot[r]]) = pv[r];
-      }
-    }
-    __syncthreads();
-    buf ^= 1;
+  };
+  for (int t0 = 0; t0 < kv_end; t0 += 2 * kPrefillBlock) {
+    step(t0, lds_k0, lds_v0, lds_k1, lds_v1);
+    if (t0 + kPrefillBlock < kv_end) step(t0 + kPrefillBlock, lds_k1, lds_v1, lds_k0, lds_v0);
   }
 
 #pragma unroll
