@@ -7,9 +7,9 @@
 // position n / g, head n % g of one KV group (g divides 16), so every column
 // carries work.  A workgroup of kPrefillWaves waves covers kPrefillCols
 // columns of one (sequence, KV head) and streams 32-token K/V blocks, up to
-// its last query position, through a double-buffered LDS tile that all its
-// waves share; the blocks are loaded straight into LDS, the next one during
-// the current one's math.  Per 16 tokens and 16 columns a wave computes
+// its last query position, through a three-stage LDS tile that all its
+// waves share; the blocks are loaded straight into LDS, two blocks ahead of
+// the math.  Per 16 tokens and 16 columns a wave computes
 //   S^T = K Q^T                 (4 MFMA 16x16x32, K rows straight from LDS)
 //   causal mask, lazy online softmax, P = P_hi + P_lo (two bf16 terms)
 //   O^T += V^T [P_hi | P_lo]^T  (8 MFMA 16x16x32: the hi and lo terms are the
@@ -49,6 +49,8 @@ constexpr int kPrefillCols = kPrefillWaves * kPrefillTiles * 16;
 constexpr int kPrefillBlock = 32;  // tokens per LDS stage
 // 16-byte chunks each thread stages per K (and per V) block
 constexpr int kPrefillLoads = kPrefillBlock * 16 / (64 * kPrefillWaves);
+// s_waitcnt vmcnt(N): all but this wave's N most recent loads (one block) have landed
+constexpr int kWaitVmcnt4p = 0x0F70 | (2 * kPrefillLoads);
 static_assert(kPrefillLoads >= 1 && kPrefillLoads * 64 * kPrefillWaves == kPrefillBlock * 16,
               "the workgroup must tile a block's chunks exactly");
 #ifndef CTX_PREFILL_XCD
@@ -72,6 +74,12 @@ typedef short s16x8 __attribute__((ext_vector_type(8)));
 // (4 tokens x 4 dimensions per 16 lanes).
 __device__ __forceinline__ int prefill_swizzle(int t) { return ((t & 7) << 1) | ((t >> 3) & 1); }
 
+// Workgroup barrier with no memory fence: the caller has already waited for
+// its own loads into LDS that the other waves will read, and a fence would
+// also wait for the loads of later blocks still in flight.  The memory clobber
+// keeps the compiler from moving LDS accesses across it.
+__device__ __forceinline__ void lds_barrier() { asm volatile("s_barrier" ::: "memory"); }
+
 // LDS transpose read: in each 16-lane group, lane l receives element l % 4 of
 // the 8-byte rows addressed by lanes l / 4, 4 + l / 4, 8 + l / 4, 12 + l / 4.
 __device__ __forceinline__ s16x4 lds_read_tr16(const uint16_t* p) {
@@ -89,7 +97,7 @@ __device__ __forceinline__ void split_bf16x2(float a, float b, uint32_t* hi, uin
 }
 
 template <typename OutT>
-__global__ __launch_bounds__(64 * kPrefillWaves) void prefill_kernel(
+__global__ __launch_bounds__(64 * kPrefillWaves) __attribute__((amdgpu_waves_per_eu(2))) void prefill_kernel(
     const uint16_t* __restrict__ q, const uint16_t* __restrict__ kc, const uint16_t* __restrict__ vc,
     const int32_t* __restrict__ offs, const int32_t* __restrict__ lens,
     const int32_t* __restrict__ q_starts, const int32_t* __restrict__ q_lens, PrefillPlan pp,
@@ -129,6 +137,8 @@ __global__ __launch_bounds__(64 * kPrefillWaves) void prefill_kernel(
   __shared__ __attribute__((aligned(16))) uint16_t lds_v0[kPrefillBlock * kHeadDim];
   __shared__ __attribute__((aligned(16))) uint16_t lds_k1[kPrefillBlock * kHeadDim];
   __shared__ __attribute__((aligned(16))) uint16_t lds_v1[kPrefillBlock * kHeadDim];
+  __shared__ __attribute__((aligned(16))) uint16_t lds_k2[kPrefillBlock * kHeadDim];
+  __shared__ __attribute__((aligned(16))) uint16_t lds_v2[kPrefillBlock * kHeadDim];
 
   // logits in log2 units are s * cs with cs >= 0: a negative scale flips the
   // sign of q instead (exact in bf16), so that max(s) * cs = max(s * cs)
@@ -186,8 +196,9 @@ __global__ __launch_bounds__(64 * kPrefillWaves) void prefill_kernel(
     dvo[r] = t * row_bytes + (((tid & 15) ^ prefill_swizzle(t)) << 4);
   }
   auto issue = [&](int tb, uint16_t* dk, uint16_t* dv) {
+    // a block past kv_end gets an empty range: no memory access, zeros in LDS
     const int rem = kv_end - tb;
-    const uint32_t bytes = (uint32_t)((rem < kPrefillBlock ? rem : kPrefillBlock) * row_bytes);
+    const uint32_t bytes = (uint32_t)((rem <= 0 ? 0 : rem < kPrefillBlock ? rem : kPrefillBlock) * row_bytes);
     const __amdgpu_buffer_rsrc_t rk = make_rsrc(kseq + (size_t)tb * row_elems, bytes);
     const __amdgpu_buffer_rsrc_t rv = make_rsrc(vseq + (size_t)tb * row_elems, bytes);
 #pragma unroll
@@ -198,6 +209,7 @@ __global__ __launch_bounds__(64 * kPrefillWaves) void prefill_kernel(
     }
   };
   issue(0, lds_k0, lds_v0);
+  issue(kPrefillBlock, lds_k1, lds_v1);
 
   // per-lane LDS offsets of the operand reads within a 16-token half block
   int k_off[4];
@@ -209,14 +221,18 @@ __global__ __launch_bounds__(64 * kPrefillWaves) void prefill_kernel(
   const int v_ch = (n & 3) >> 1;
 
   // One 32-token block: wait for this wave's loads of it, then the barrier
-  // (every wave's loads have landed, and every wave is done with the other
-  // stage); the next block's loads go into that stage during this block's
-  // math.  The two stages are distinct LDS arrays named at compile time, so
-  // the compiler's wait before the reads covers only this stage's loads.
+  // (every wave's loads have landed, and every wave is done with the stage
+  // read in the previous step); the loads of the block two ahead go into that
+  // stage, in flight for two steps of math.  The three stages are distinct LDS
+  // arrays named at compile time, so the compiler's wait before the reads
+  // covers only this stage's loads.
   auto step = [&](int t0, const uint16_t* kt, const uint16_t* vt, uint16_t* nk, uint16_t* nv) {
-    __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
-    __syncthreads();
-    if (t0 + kPrefillBlock < kv_end) issue(t0 + kPrefillBlock, nk, nv);
+    // Every step issues the loads of the block two ahead (an empty range past
+    // kv_end), so this wave's loads of this block are all but its newest
+    // block's worth; the barrier then makes everyone's visible.
+    __builtin_amdgcn_s_waitcnt(kWaitVmcnt4p);
+    lds_barrier();
+    issue(t0 + 2 * kPrefillBlock, nk, nv);
     if (wave_active && t0 < wave_end) {
       // S^T of tokens t0 + 16 h + 4c + i (i < 4) for every column tile
       f32x4 sc[kPrefillTiles][2];
@@ -302,10 +318,16 @@ __global__ __launch_bounds__(64 * kPrefillWaves) void prefill_kernel(
       __builtin_amdgcn_s_setprio(0);
     }
   };
-  for (int t0 = 0; t0 < kv_end; t0 += 2 * kPrefillBlock) {
-    step(t0, lds_k0, lds_v0, lds_k1, lds_v1);
-    if (t0 + kPrefillBlock < kv_end) step(t0 + kPrefillBlock, lds_k1, lds_v1, lds_k0, lds_v0);
+  // block j in stage j % 3; step j issues block j + 2 into stage (j + 2) % 3
+  for (int t0 = 0; t0 < kv_end; t0 += 3 * kPrefillBlock) {
+    step(t0, lds_k0, lds_v0, lds_k2, lds_v2);
+    if (t0 + kPrefillBlock >= kv_end) break;
+    step(t0 + kPrefillBlock, lds_k1, lds_v1, lds_k0, lds_v0);
+    if (t0 + 2 * kPrefillBlock >= kv_end) break;
+    step(t0 + 2 * kPrefillBlock, lds_k2, lds_v2, lds_k1, lds_v1);
   }
+  // no load may land in LDS after the workgroup has released it
+  __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
 
 #pragma unroll
   for (int ct = 0; ct < kPrefillTiles; ++ct) {
