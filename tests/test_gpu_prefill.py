@@ -160,3 +160,23 @@ def test_prefill_bf16_output():
     rows = np.concatenate([np.arange(qs[b], qs[b] + nq[b]) for b in range(5)])
     want = wl.bf16_bits_to_f32(wl.f32_to_bf16_bits(f32[rows].astype(np.float32)))
     np.testing.assert_array_equal(b16[rows], want)
+
+
+def test_prefill_block_boundaries():
+    """Contexts that end on, just before and just after the 32-token K/V
+    blocks the workgroup streams (1, 31, 32, 33, 64, 65, 96, 97 tokens), as
+    fresh prompts and with a short history: the last blocks' loads, the loads
+    issued past the end and the final drain."""
+    rng = np.random.default_rng(77)
+    ends = np.array([1, 31, 32, 33, 64, 65, 96, 97], np.int32)
+    batch = 2 * len(ends)
+    lens = np.concatenate([ends, ends]).astype(np.int32)
+    nq = np.concatenate([ends, np.minimum(ends, 5)]).astype(np.int32)  # fresh prompts, then 5 new tokens
+    lay = wl.make_layout(lens, 1, gap_max=5, shuffle=True, rng=rng)
+    w = wl.Workload("pfedge", 191, 1, batch, 32, 8, 1, "uniform", 1, 2)
+    k, v = wl.layer_kv_bits(w, lay, 0, fill=wl.BF16_NAN)
+    q_starts = np.concatenate([[0], np.cumsum(nq)[:-1]]).astype(np.int32)
+    q = rand_bits(rng, (int(nq.sum()), 32, 128))
+    ref = oracle.prefill_attn(q, k, v, lay.offsets, lens, q_starts, nq, w.scale)
+    got = run_prefill(w, lay, lens, nq, q_starts, q, k, v)
+    assert_parity(got, ref, "block boundaries")
