@@ -57,22 +57,24 @@ __device__ __forceinline__ s16x4 pack_bf16x4(float a, float b, float c, float d)
 
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 
-#ifndef CTX_NT_LOADS
-#define CTX_NT_LOADS 1
-#endif
+// LDS transpose read (gfx950): in each 16-lane group, lane l receives element
+// l % 4 of the 8-byte rows addressed by lanes l / 4, 4 + l / 4, 8 + l / 4 and
+// 12 + l / 4 -- four tokens of one dimension when those rows are four
+// dimensions of four consecutive tokens.
+__device__ __forceinline__ s16x4 lds_read_tr16(const uint16_t* p) {
+  typedef s16x4 __attribute__((address_space(3))) * lds_s16x4;
+  return __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4)(p));
+}
 
+// 16-byte load of data read once (non-temporal)
 __device__ __forceinline__ u32x4 load16(const uint16_t* p) {
-#if CTX_NT_LOADS
   return __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(p));
-#else
-  return *reinterpret_cast<const u32x4*>(p);
-#endif
 }
 
 // Buffer resources: a wave-uniform base and byte size; loads past the size
 // return zeros, which covers the ragged last block of a segment.
 constexpr int kRsrcWord3 = 0x00020000;  // raw buffer, 32-bit data format
-constexpr int kLoadAux = CTX_NT_LOADS ? 2 : 0;  // 2 = non-temporal (streamed once)
+constexpr int kLoadAux = 2;  // cache policy of streamed K/V loads: non-temporal (read once)
 
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const uint16_t* base, uint32_t bytes) {
   const uint64_t a = reinterpret_cast<uint64_t>(base);

@@ -429,10 +429,7 @@ __device__ __forceinline__ float lane_value(float x, int src) {
 // weights are computed one segment per lane; partial outputs are read in
 // batches of kMergeBatch segments, the next batch in flight while the current
 // one is accumulated.
-#ifndef CTX_MERGE_BATCH
-#define CTX_MERGE_BATCH 16
-#endif
-constexpr int kMergeBatch = CTX_MERGE_BATCH;
+constexpr int kMergeBatch = 16;
 
 __device__ __forceinline__ void load_partials(float2 (&dst)[kMergeBatch], const float* __restrict__ o_ws,
                                               size_t first, size_t stride, int s0, int cnt, int lane) {

@@ -27,24 +27,14 @@
 
 namespace {
 
-// Cached variant for data that several workgroups re-read (prefill tiles).
-#ifndef CTX_PREFILL_AUX
-#define CTX_PREFILL_AUX 0
-#endif
-__device__ __forceinline__ u32x4 buf_load16_shared(__amdgpu_buffer_rsrc_t r, int voff, int soff) {
-  return __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, CTX_PREFILL_AUX));
-}
+// K/V block loads use the default (cached) policy: the query tiles of one
+// (sequence, KV head) re-read the same blocks, mostly from L2.
+constexpr int kPrefillLoadAux = 0;
 
 constexpr int kWaitVmcnt0 = 0x0F70;  // s_waitcnt vmcnt(0), expcnt and lgkmcnt left open
 typedef __attribute__((address_space(3))) void lds_void;
-#ifndef CTX_PREFILL_WAVES
-#define CTX_PREFILL_WAVES 4
-#endif
-constexpr int kPrefillWaves = CTX_PREFILL_WAVES;
-#ifndef CTX_PREFILL_TILES
-#define CTX_PREFILL_TILES 3
-#endif
-constexpr int kPrefillTiles = CTX_PREFILL_TILES;  // 16-column tiles per wave
+constexpr int kPrefillWaves = 4;  // waves per workgroup
+constexpr int kPrefillTiles = 3;  // 16-column tiles per wave
 constexpr int kPrefillCols = kPrefillWaves * kPrefillTiles * 16;
 constexpr int kPrefillBlock = 32;  // tokens per LDS stage
 // 16-byte chunks each thread stages per K (and per V) block
@@ -53,9 +43,6 @@ constexpr int kPrefillLoads = kPrefillBlock * 16 / (64 * kPrefillWaves);
 constexpr int kWaitVmcnt4p = 0x0F70 | (2 * kPrefillLoads);
 static_assert(kPrefillLoads >= 1 && kPrefillLoads * 64 * kPrefillWaves == kPrefillBlock * 16,
               "the workgroup must tile a block's chunks exactly");
-#ifndef CTX_PREFILL_XCD
-#define CTX_PREFILL_XCD 1
-#endif
 
 struct PrefillPlan {
   int32_t hq;
@@ -65,8 +52,6 @@ struct PrefillPlan {
   int32_t units;  // sequences x KV heads
   float scale_log2;
 };
-
-typedef short s16x8 __attribute__((ext_vector_type(8)));
 
 // LDS tile of K or V: token row t holds its 16 chunks of 8 dimensions with
 // chunk ch at slot ch ^ prefill_swizzle(t): conflict-free for the staging
@@ -79,13 +64,6 @@ __device__ __forceinline__ int prefill_swizzle(int t) { return ((t & 7) << 1) | 
 // also wait for the loads of later blocks still in flight.  The memory clobber
 // keeps the compiler from moving LDS accesses across it.
 __device__ __forceinline__ void lds_barrier() { asm volatile("s_barrier" ::: "memory"); }
-
-// LDS transpose read: in each 16-lane group, lane l receives element l % 4 of
-// the 8-byte rows addressed by lanes l / 4, 4 + l / 4, 8 + l / 4, 12 + l / 4.
-__device__ __forceinline__ s16x4 lds_read_tr16(const uint16_t* p) {
-  typedef s16x4 __attribute__((address_space(3))) * lds_s16x4;
-  return __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4)(p));
-}
 
 // Split a pair of non-negative floats into bf16 hi = the value with its low 16
 // bits cleared and bf16 lo = round-to-nearest-even of the exact remainder, so
@@ -108,17 +86,12 @@ __global__ __launch_bounds__(64 * kPrefillWaves) __attribute__((amdgpu_waves_per
   const int n = lane & 15;
   const int c = lane >> 4;
   const int g = pp.group;
-#if CTX_PREFILL_XCD
   // consecutive workgroups go to different XCDs; keep every tile of a unit on
   // one XCD so that its L2 serves the tiles' re-reads of the unit's K/V
   const int slot = blockIdx.x / kXcds;
   const int tile = slot % pp.tiles;
   const int unit = (slot / pp.tiles) * kXcds + (int)(blockIdx.x % kXcds);
   if (unit >= pp.units) return;
-#else
-  const int tile = blockIdx.x % pp.tiles;
-  const int unit = blockIdx.x / pp.tiles;
-#endif
   const int kv = unit % pp.hkv;
   const int b = unit / pp.hkv;
   const int nq = q_lens[b];
@@ -204,8 +177,8 @@ __global__ __launch_bounds__(64 * kPrefillWaves) __attribute__((amdgpu_waves_per
 #pragma unroll
     for (int r = 0; r < kPrefillLoads; ++r) {
       const int row0 = r * 4 * kPrefillWaves + 4 * wave;  // first token row of this wave's round
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(rk, (lds_void*)&dk[row0 * kHeadDim], 16, dvo[r], 0, 0, CTX_PREFILL_AUX);
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(rv, (lds_void*)&dv[row0 * kHeadDim], 16, dvo[r], 0, 0, CTX_PREFILL_AUX);
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rk, (lds_void*)&dk[row0 * kHeadDim], 16, dvo[r], 0, 0, kPrefillLoadAux);
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rv, (lds_void*)&dv[row0 * kHeadDim], 16, dvo[r], 0, 0, kPrefillLoadAux);
     }
   };
   issue(0, lds_k0, lds_v0);
@@ -370,7 +343,7 @@ extern "C" int ctx_prefill_attn_run(ctx_decode_attn* h, const void* q, const voi
   pp.tiles = (int32_t)(((int64_t)max_q_len * g + kPrefillCols - 1) / kPrefillCols);
   pp.scale_log2 = (float)((double)scale * 1.4426950408889634);
   pp.units = num_seqs * d.num_kv_heads;
-  const int64_t blocks = (CTX_PREFILL_XCD ? round_up(pp.units, kXcds) : (int64_t)pp.units) * pp.tiles;
+  const int64_t blocks = round_up(pp.units, kXcds) * pp.tiles;  // units padded to whole XCD rounds
   if (blocks > INT32_MAX) return fail(CTX_ERR_INVALID_ARG, "prefill grid too large");
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
   const uint16_t* qp = static_cast<const uint16_t*>(q);
