@@ -5,6 +5,8 @@ import os
 import shutil
 import subprocess
 import sys
+import tempfile
+from concurrent.futures import ThreadPoolExecutor
 
 PKG = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(PKG)
@@ -34,18 +36,47 @@ def compile_flags() -> list[str]:
             "-I", INCLUDE]
 
 
-def build(verbose: bool = False, extra: list[str] | None = None, out: str | None = None) -> str:
-    out = out or LIB
-    cmd = [hipcc(), *compile_flags(), *(extra or []), "-shared", "-o", out + ".tmp", *SRCS]
+# Extra device-compiler flags per source file.
+FILE_FLAGS = {
+    # The OPD row kernel holds a row's 16-byte chunks in a small array indexed
+    # by the unrolled chunk loops.  Promoting that array to one vector value
+    # made the instantiations for up to 8 chunks per thread spill hundreds of
+    # VGPRs; kept as separate registers they need 44-64.
+    "ctx_opd_loss.hip": ["-mllvm", "-disable-promote-alloca-to-vector"],
+}
+BUILD_DIR = os.path.join(PKG, "_build")
+_NOISE = "is not a recognized feature for this target"
+
+
+def _run(cmd: list[str], verbose: bool) -> None:
     if verbose:
         print(" ".join(cmd), flush=True)
     res = subprocess.run(cmd, capture_output=True, text=True)
-    noise = "is not a recognized feature for this target"
-    msgs = [l for l in (res.stdout + res.stderr).splitlines() if noise not in l]
+    msgs = [l for l in (res.stdout + res.stderr).splitlines() if _NOISE not in l]
     if msgs and (verbose or res.returncode):
         print("\n".join(msgs), file=sys.stderr, flush=True)
     if res.returncode != 0:
-        raise RuntimeError(f"hipcc failed ({res.returncode})")
+        raise RuntimeError(f"hipcc failed ({res.returncode}): {' '.join(cmd[-3:])}")
+
+
+def build(verbose: bool = False, extra: list[str] | None = None, out: str | None = None) -> str:
+    """Compile every source to an object (in parallel, each with its own extra
+    flags), then link the shared library `out` (default: the in-tree library)."""
+    out = out or LIB
+    os.makedirs(BUILD_DIR, exist_ok=True)
+    objdir = tempfile.mkdtemp(dir=BUILD_DIR)
+    try:
+        def compile_one(src: str) -> str:
+            obj = os.path.join(objdir, os.path.basename(src) + ".o")
+            _run([hipcc(), *compile_flags(), *FILE_FLAGS.get(os.path.basename(src), []), *(extra or []),
+                  "-c", src, "-o", obj], verbose)
+            return obj
+
+        with ThreadPoolExecutor(max_workers=len(SRCS)) as pool:
+            objs = list(pool.map(compile_one, SRCS))
+        _run([hipcc(), f"--offload-arch={ARCH}", "-shared", "-fPIC", "-o", out + ".tmp", *objs], verbose)
+    finally:
+        shutil.rmtree(objdir, ignore_errors=True)
     os.replace(out + ".tmp", out)
     return out
 
