@@ -586,7 +586,11 @@ def main() -> int:
     ap.add_argument("--steps", type=int, default=64, help="decode steps timed (each = all layers)")
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="long_ragged", choices=sorted(wl.WORKLOADS))
-    ap.add_argument("--graph", action="store_true", help="replay the timed steps from one HIP graph")
+    ap.add_argument("--launch", choices=("both", "stream", "graph"), default="both",
+                    help="decode: time stream launches, a HIP-graph replay of the same steps, or both "
+                         "(default; `value` is then the graph replay)")
+    ap.add_argument("--graph", action="store_const", dest="launch", const="graph",
+                    help="decode: time the HIP-graph replay only")
     ap.add_argument("--paged", type=int, default=0, metavar="P",
                     help="use P-token pages (shuffled block tables) and append each step's token")
     ap.add_argument("--prefill", action="store_true",
@@ -699,35 +703,46 @@ def main() -> int:
         step(i)
     torch.cuda.synchronize()
 
-    graph = None
-    if args.graph:
-        graph = torch.cuda.CUDAGraph()
-        side = torch.cuda.Stream()
-        side.wait_stream(stream)
-        with torch.cuda.stream(side):
-            with torch.cuda.graph(graph, stream=side):
-                saved = stream
-                stream = side
-                for s in range(args.steps):
-                    step(s)
-                stream = saved
+    def time_steps(use_graph: bool) -> float:
+        """Seconds for exactly args.steps decode steps (all layers), HIP events on
+        the launch stream; with use_graph the steps are captured once and the
+        graph is replayed (after one untimed warm replay)."""
+        nonlocal stream
+        graph = None
+        if use_graph:
+            graph = torch.cuda.CUDAGraph()
+            side = torch.cuda.Stream()
+            side.wait_stream(stream)
+            with torch.cuda.stream(side):
+                with torch.cuda.graph(graph, stream=side):
+                    saved = stream
+                    stream = side
+                    for s in range(args.steps):
+                        step(s)
+                    stream = saved
+            torch.cuda.synchronize()
+            graph.replay()  # warm replay
+            torch.cuda.synchronize()
+        start = torch.cuda.Event(enable_timing=True)
+        stop = torch.cuda.Event(enable_timing=True)
         torch.cuda.synchronize()
-        graph.replay()  # warm replay
+        start.record(stream)
+        if graph is not None:
+            graph.replay()
+        else:
+            for s in range(args.steps):
+                step(s)
+        stop.record(stream)
+        stop.synchronize()
         torch.cuda.synchronize()
+        return start.elapsed_time(stop) / 1e3
 
-    start = torch.cuda.Event(enable_timing=True)
-    stop = torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
-    start.record(stream)
-    if graph is not None:
-        graph.replay()
-    else:
-        for s in range(args.steps):
-            step(s)
-    stop.record(stream)
-    stop.synchronize()
-    torch.cuda.synchronize()
-    elapsed_s = start.elapsed_time(stop) / 1e3
+    # stream launches, then (by default) the same steps replayed from one graph,
+    # the way a serving engine runs its decode steps; `value` is the graph replay
+    modes = {"both": (True, True), "stream": (True, False), "graph": (False, True)}[args.launch]
+    stream_s = time_steps(False) if modes[0] else None
+    graph_s = time_steps(True) if modes[1] else None
+    elapsed_s = graph_s if graph_s is not None else stream_s
 
     step_bytes = [algorithmic_bytes(layout.lens_at(s % w.steps), w) * w.layers for s in range(args.steps)]
     total_bytes = float(sum(step_bytes))
@@ -770,7 +785,7 @@ def main() -> int:
             "tokens_per_layer_step0": int(layout.lens.sum()),
             "distinct_layer_buffers": n_buf,
             "seed": wl.DEFAULT_SEED,
-            "launch": "hip_graph" if graph is not None else "stream",
+            "launch": "hip_graph" if graph_s is not None else "stream",
             "kv_layout": f"paged, {args.paged}-token pages, appends each step's token" if args.paged else "contiguous",
             "parallelism": "none (1 GPU)",
         },
@@ -790,6 +805,12 @@ def main() -> int:
         },
         "setup_s": round(setup_s, 1),
     }
+    if graph_s is not None and stream_s is not None:
+        result["stream_launches"] = {
+            "value": round(total_bytes / stream_s / 1e9, 2),
+            "ms_per_step": round(stream_s * 1e3 / args.steps, 4),
+            "avg_launch_us": round(stream_s / calls * 1e6, 3),
+        }
     if not args.no_cpu_baseline:
         threads = len(os.sched_getaffinity(0))
         result["cpu_baseline"] = cpu_baseline(w, layout, args.cpu_seconds, threads)
