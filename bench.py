@@ -607,8 +607,8 @@ def main() -> int:
     args = ap.parse_args()
 
     if args.gpus != 1:
-        print(f"bench.py: this build measures one GPU only (got --gpus {args.gpus}); the decode "
-              f"attention shards by sequence with no exchange, so run one process per GPU.",
+        print(f"bench.py measures one GPU (got --gpus {args.gpus}): the decode attention shards by "
+              f"sequence with no exchange between GPUs, so run one process per GPU.",
               file=sys.stderr)
         return 2
     if args.steps < 1 or args.warmup < 0:
