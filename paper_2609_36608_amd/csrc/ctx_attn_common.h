@@ -24,6 +24,7 @@ struct ctx_decode_attn {
   int num_cus;
   int32_t ranges_auto;  // ranges of the balanced split
   int64_t max_ranges;   // most ranges any run call can use
+  int32_t split_wgw;    // waves (KV heads of one range) per split workgroup
   float* o_ws;
   float2* ml_ws;
 };

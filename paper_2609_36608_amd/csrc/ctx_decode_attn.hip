@@ -7,9 +7,9 @@
 //
 // Design (flash-decoding split-K, register resident):
 //   * Work split.  The batch's tokens, flattened sequence after sequence, are
-//     cut into equal ranges, one range per group of Hkv single-wave
-//     workgroups (one wave per KV head), sized so the whole grid is resident
-//     at once.  Every wave derives its ranges from seq_lens on the device,
+//     cut into equal ranges, one wave per (range, KV head), sized so the
+//     whole grid is resident at once; a workgroup holds the waves of up to 4
+//     KV heads of one range, each with its own LDS tiles.  Every wave derives its ranges from seq_lens on the device,
 //     so no host sync is needed and the call is graph-capturable.  A range
 //     that holds a whole sequence writes that sequence's output directly;
 //     otherwise each piece writes an fp32 partial (m, l, o) to the workspace
@@ -50,6 +50,8 @@ constexpr int kBlock = 16;        // tokens per MFMA block
 constexpr int kMaxGroup = 16;     // query heads per KV head (MFMA N dimension)
 constexpr int kMinRange = 64;     // smallest balanced range, tokens
 constexpr int kMergeWaves = 4;
+constexpr int kWgWaves = 4;  // most waves (KV heads of one range) per split workgroup
+constexpr int kTileBytes = 2 * kBlock * kHeadDim * 2;  // one wave's K and V tiles in LDS
 #ifndef CTX_WAVES_PER_EU
 #define CTX_WAVES_PER_EU 3
 #endif
@@ -225,24 +227,32 @@ __device__ __forceinline__ void attend_block(const u32x4 (&kr)[4], const u32x4 (
 // ------------------------------------------------------------ split kernel
 
 template <typename OutT, bool kPaged>
-__global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(CTX_WAVES_PER_EU))) void decode_split_kernel(
+__global__ __launch_bounds__(64 * kWgWaves) __attribute__((amdgpu_waves_per_eu(CTX_WAVES_PER_EU))) void decode_split_kernel(
     const uint16_t* __restrict__ q, const uint16_t* __restrict__ kc,
     const uint16_t* __restrict__ vc, const int32_t* __restrict__ offs,
     const int32_t* __restrict__ lens, Plan p, Paged pg, float* __restrict__ o_ws,
     float2* __restrict__ ml_ws, OutT* __restrict__ out) {
-  const int lane = threadIdx.x;
+  const int lane = threadIdx.x & 63;
   const int n = lane & 15;
   const int c = lane >> 4;
-  // Range-major order: consecutive workgroups take consecutive ranges of one
-  // KV head.  Workgroups are dealt round-robin over the XCDs (id % kXcds) and
-  // num_ranges % kXcds == 0, so every head of a range lands on the same XCD
-  // (range w on XCD w % kXcds) while each CU holds the same head of nearby
-  // ranges.  Measured on MI355X this order streams the cache fastest.
-  const int kv = blockIdx.x / p.num_ranges;
-  const int w = blockIdx.x - kv * p.num_ranges;
+  // A workgroup holds wgw waves, KV heads hg * wgw .. hg * wgw + wgw - 1 of
+  // one range w, so that a CU reads several heads' slices of the same token
+  // rows at once.  Range-major order: consecutive workgroups take consecutive
+  // ranges of one head group.  Workgroups are dealt round-robin over the XCDs
+  // (id % kXcds) and num_ranges % kXcds == 0, so every head of a range lands on
+  // the same XCD (range w on XCD w % kXcds).  Measured on MI355X this order
+  // streams the cache fastest.
+  const int wgw = (int)(blockDim.x >> 6);
+  const int wv = __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
+  const int hg = blockIdx.x / p.num_ranges;
+  const int w = blockIdx.x - hg * p.num_ranges;
+  const int kv = hg * wgw + wv;
   const int g = p.group;
-  __shared__ __attribute__((aligned(16))) uint16_t lds_k[kBlock * kHeadDim];
-  __shared__ __attribute__((aligned(16))) uint16_t lds_v[kBlock * kHeadDim];
+  // each wave owns a K and a V tile in the workgroup's (dynamic) LDS; its LDS
+  // instructions execute in order, so staging a block needs no barrier
+  extern __shared__ __attribute__((aligned(16))) uint16_t lds_tiles[];
+  uint16_t* lds_k = lds_tiles + (size_t)wv * (kTileBytes / 2);
+  uint16_t* lds_v = lds_k + kBlock * kHeadDim;
 
   // this wave's token range [ws, we) and the first sequence b it overlaps (span starts at pos)
   int64_t total, width, ws, pos;
@@ -359,7 +369,7 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(CTX_WAVES_PE
           pk[u] = buf_load16(rk, voff, 4 * u * row_bytes);
           pv[u] = buf_load16(rv, voff, 4 * u * row_bytes);
         }
-        __syncthreads();  // previous block's LDS reads are done
+        __builtin_amdgcn_wave_barrier();  // keep the previous block's LDS reads before these writes
 #pragma unroll
         for (int u = 0; u < 4; ++u) {
           const int tok = 4 * u + ld_tok;
@@ -383,7 +393,7 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(CTX_WAVES_PE
             *reinterpret_cast<u32x4*>(pg.v_cache + dst) = nv;
           }
         }
-        __syncthreads();
+        __builtin_amdgcn_wave_barrier();
         u32x4 kr[4], vr[4];
 #pragma unroll
         for (int kk = 0; kk < 4; ++kk) {
@@ -580,7 +590,10 @@ int ctx_decode_attn_create(const ctx_decode_attn_desc* desc, ctx_decode_attn** o
   int cus = 0;
   e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
   if (e != hipSuccess) return hip_fail(e, "hipDeviceGetAttribute");
-  // resident single-wave workgroups per CU: the smaller of the two layouts' kernels
+  // Workgroups hold the KV heads of one range: 4, 2 or 1 of them (a divisor of
+  // Hkv).  Resident waves per CU: the smaller of the two layouts' kernels.
+  int wgw = kWgWaves;
+  while (d.num_kv_heads % wgw != 0) wgw >>= 1;
   const void* kernels[2] = {
       d.out_dtype == CTX_DTYPE_F32 ? reinterpret_cast<const void*>(&decode_split_kernel<float, false>)
                                    : reinterpret_cast<const void*>(&decode_split_kernel<uint16_t, false>),
@@ -589,8 +602,9 @@ int ctx_decode_attn_create(const ctx_decode_attn_desc* desc, ctx_decode_attn** o
   int per_cu = 1 << 30;
   for (const void* kern : kernels) {
     int n = 0;
-    e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, kern, 64, 0);
+    e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, kern, 64 * wgw, (size_t)wgw * kTileBytes);
     if (e != hipSuccess) return hip_fail(e, "hipOccupancyMaxActiveBlocksPerMultiprocessor");
+    n *= wgw;  // waves
     if (n < per_cu) per_cu = n;
   }
   if (per_cu < 1) per_cu = 1;
@@ -617,6 +631,7 @@ int ctx_decode_attn_create(const ctx_decode_attn_desc* desc, ctx_decode_attn** o
   h->num_cus = cus;
   h->ranges_auto = (int32_t)ranges_auto;
   h->max_ranges = max_ranges;
+  h->split_wgw = wgw;
   e = hipMalloc(reinterpret_cast<void**>(&h->o_ws), o_bytes);
   if (e == hipSuccess) e = hipMalloc(reinterpret_cast<void**>(&h->ml_ws), ml_bytes);
   if (e != hipSuccess) {
@@ -651,20 +666,22 @@ int launch(ctx_decode_attn* h, const void* q, const void* k, const void* v, cons
   p.scale_log2 = (float)((double)scale * 1.4426950408889634);
 
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
-  const dim3 split_grid((unsigned)(p.num_ranges * p.hkv));
+  const int wgw = h->split_wgw;
+  const size_t split_lds = (size_t)wgw * kTileBytes;
+  const dim3 split_grid((unsigned)(p.num_ranges * p.hkv / wgw));
   const dim3 merge_grid((unsigned)(((int64_t)num_seqs * p.hq + kMergeWaves - 1) / kMergeWaves));
   const uint16_t* qp = static_cast<const uint16_t*>(q);
   const uint16_t* kp = static_cast<const uint16_t*>(k);
   const uint16_t* vp = static_cast<const uint16_t*>(v);
   if (d.out_dtype == CTX_DTYPE_F32) {
     float* op = static_cast<float*>(out);
-    hipLaunchKernelGGL((decode_split_kernel<float, kPaged>), split_grid, dim3(64), 0, s, qp, kp, vp, offs,
-                       lens, p, pg, h->o_ws, h->ml_ws, op);
+    hipLaunchKernelGGL((decode_split_kernel<float, kPaged>), split_grid, dim3(64 * wgw), split_lds, s, qp, kp, vp,
+                       offs, lens, p, pg, h->o_ws, h->ml_ws, op);
     hipLaunchKernelGGL(decode_merge_kernel<float>, merge_grid, dim3(64 * kMergeWaves), 0, s, lens, p,
                        h->o_ws, h->ml_ws, op);
   } else {
     uint16_t* op = static_cast<uint16_t*>(out);
-    hipLaunchKernelGGL((decode_split_kernel<uint16_t, kPaged>), split_grid, dim3(64), 0, s, qp, kp, vp,
+    hipLaunchKernelGGL((decode_split_kernel<uint16_t, kPaged>), split_grid, dim3(64 * wgw), split_lds, s, qp, kp, vp,
                        offs, lens, p, pg, h->o_ws, h->ml_ws, op);
     hipLaunchKernelGGL(decode_merge_kernel<uint16_t>, merge_grid, dim3(64 * kMergeWaves), 0, s, lens, p,
                        h->o_ws, h->ml_ws, op);
