@@ -88,7 +88,8 @@ def test_spike_retrieval_exact_rows():
 def test_gqa_mapping_exact():
     """V = kv index on each KV head -> out[b, h, :] = h // g for every group size."""
     rng = np.random.default_rng(23)
-    for hq, hkv in [(32, 8), (16, 8), (8, 8), (16, 1), (32, 2), (64, 4)]:
+    # Hkv 8, 4 -> four KV heads per workgroup; 2, 6 -> two; 1, 3 -> one
+    for hq, hkv in [(32, 8), (16, 8), (8, 8), (16, 1), (32, 2), (64, 4), (12, 6), (12, 3)]:
         lens = np.array([3, 40, 129], np.int32)
         lay = wl.make_layout(lens, 1)
         k = rand_bits(rng, (lay.num_rows, hkv, 128))

@@ -180,3 +180,24 @@ def test_prefill_block_boundaries():
     ref = oracle.prefill_attn(q, k, v, lay.offsets, lens, q_starts, nq, w.scale)
     got = run_prefill(w, lay, lens, nq, q_starts, q, k, v)
     assert_parity(got, ref, "block boundaries")
+
+
+def test_prefill_sequences_without_new_tokens():
+    """Sequences with no new tokens produce nothing (their rows stay untouched),
+    and a max_q_len above the batch's longest only adds idle workgroups."""
+    w, lay, lens, nq, qs, q, k, v = prefill_case(41, 32, 8, batch=6, hist=(20, 400), new=(1, 90))
+    nq[1] = 0
+    nq[4] = 0
+    ref = oracle.prefill_attn(q, k, v, lay.offsets, lens, qs, nq, w.scale)
+    total_q = q.shape[0]
+    with DecodeAttention(32, 8, 6, int(lens.max())) as attn:
+        out = torch.full((total_q, 32, 128), -555.0, dtype=torch.float32, device=dev())
+        attn.prefill(up_bf16(q), up_bf16(k), up_bf16(v), up_i32(lay.offsets), up_i32(lens), up_i32(qs),
+                     up_i32(nq), int(nq.max()) + 200, w.scale, out)
+        torch.cuda.synchronize()
+    got = out.cpu().numpy()
+    rows = np.zeros(total_q, bool)
+    for b in range(6):
+        rows[qs[b]:qs[b] + nq[b]] = True
+    assert_parity(got[rows], ref[rows], "with empty sequences")
+    assert (got[~rows] == -555.0).all(), "rows of sequences without new tokens were written"
