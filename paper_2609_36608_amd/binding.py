@@ -144,6 +144,26 @@ def _dtype_code(dtype) -> int:
     raise ValueError(f"out dtype must be float32 or bfloat16, not {dtype}")
 
 
+def _check_tensors(device: int, checks) -> None:
+    """Each (name, tensor, dtype): that dtype, on cuda:device, contiguous."""
+    for name, t, dt in checks:
+        if t.dtype != dt:
+            raise TypeError(f"{name} must be {dt}, got {t.dtype}")
+        if not t.is_cuda or t.device.index != device:
+            raise ValueError(f"{name} must be on cuda:{device}")
+        if not t.is_contiguous():
+            raise ValueError(f"{name} must be contiguous")
+
+
+def _stream_ptr(stream, device=None) -> int:
+    """hipStream_t of a torch stream (default: the current one of `device`) or a raw handle."""
+    import torch
+
+    if stream is None:
+        stream = torch.cuda.current_stream(device)
+    return stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream)
+
+
 class DecodeAttention:
     """Handle for ctx_decode_attn_run: decode-step GQA attention of one new token
     per sequence over ragged KV caches [rows, Hkv, 128] (bf16)."""
@@ -169,15 +189,9 @@ class DecodeAttention:
         if self.handle is None:
             raise RuntimeError("handle is closed")
         d = self.desc
-        for name, t, dt in (("q", q, torch.bfloat16), ("k_cache", k_cache, torch.bfloat16),
-                            ("v_cache", v_cache, torch.bfloat16), ("seq_offsets", seq_offsets, torch.int32),
-                            ("seq_lens", seq_lens, torch.int32), ("out", out, self.out_dtype)):
-            if t.dtype != dt:
-                raise TypeError(f"{name} must be {dt}, got {t.dtype}")
-            if not t.is_cuda or t.device.index != self.device:
-                raise ValueError(f"{name} must be on cuda:{self.device}")
-            if not t.is_contiguous():
-                raise ValueError(f"{name} must be contiguous")
+        _check_tensors(self.device, (("q", q, torch.bfloat16), ("k_cache", k_cache, torch.bfloat16),
+                                     ("v_cache", v_cache, torch.bfloat16), ("seq_offsets", seq_offsets, torch.int32),
+                                     ("seq_lens", seq_lens, torch.int32), ("out", out, self.out_dtype)))
         b = q.shape[0]
         if q.shape != (b, d.num_q_heads, d.head_dim) or out.shape != q.shape:
             raise ValueError(f"q/out must be [{b}, {d.num_q_heads}, {d.head_dim}]")
@@ -185,9 +199,7 @@ class DecodeAttention:
             raise ValueError(f"k_cache/v_cache must be [rows, {d.num_kv_heads}, {d.head_dim}]")
         if seq_offsets.shape != (b,) or seq_lens.shape != (b,):
             raise ValueError(f"seq_offsets/seq_lens must be [{b}]")
-        if stream is None:
-            stream = torch.cuda.current_stream()
-        sp = stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream)
+        sp = _stream_ptr(stream)
         rc = self.lib.ctx_decode_attn_run(self.handle, q.data_ptr(), k_cache.data_ptr(), v_cache.data_ptr(),
                                           seq_offsets.data_ptr(), seq_lens.data_ptr(), b, float(scale),
                                           out.data_ptr(), sp)
@@ -212,13 +224,7 @@ class DecodeAttention:
                   ("seq_lens", seq_lens, torch.int32), ("out", out, self.out_dtype)]
         if k_new is not None:
             checks += [("k_new", k_new, torch.bfloat16), ("v_new", v_new, torch.bfloat16)]
-        for name, t, dt in checks:
-            if t.dtype != dt:
-                raise TypeError(f"{name} must be {dt}, got {t.dtype}")
-            if not t.is_cuda or t.device.index != self.device:
-                raise ValueError(f"{name} must be on cuda:{self.device}")
-            if not t.is_contiguous():
-                raise ValueError(f"{name} must be contiguous")
+        _check_tensors(self.device, checks)
         b = q.shape[0]
         if q.shape != (b, d.num_q_heads, d.head_dim) or out.shape != q.shape:
             raise ValueError(f"q/out must be [{b}, {d.num_q_heads}, {d.head_dim}]")
@@ -229,9 +235,7 @@ class DecodeAttention:
             raise ValueError(f"block_tables must be [{b}, max_pages] and seq_lens [{b}]")
         if k_new is not None and (k_new.shape != (b, d.num_kv_heads, d.head_dim) or v_new.shape != k_new.shape):
             raise ValueError(f"k_new/v_new must be [{b}, {d.num_kv_heads}, {d.head_dim}]")
-        if stream is None:
-            stream = torch.cuda.current_stream()
-        sp = stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream)
+        sp = _stream_ptr(stream)
         rc = self.lib.ctx_decode_attn_run_paged(
             self.handle, q.data_ptr(), k_pages.data_ptr(), v_pages.data_ptr(), block_tables.data_ptr(),
             block_tables.shape[1], seq_lens.data_ptr(), b,
@@ -250,16 +254,10 @@ class DecodeAttention:
         if self.handle is None:
             raise RuntimeError("handle is closed")
         d = self.desc
-        for name, t, dt in (("q", q, torch.bfloat16), ("k_cache", k_cache, torch.bfloat16),
-                            ("v_cache", v_cache, torch.bfloat16), ("seq_offsets", seq_offsets, torch.int32),
-                            ("seq_lens", seq_lens, torch.int32), ("q_starts", q_starts, torch.int32),
-                            ("q_lens", q_lens, torch.int32), ("out", out, self.out_dtype)):
-            if t.dtype != dt:
-                raise TypeError(f"{name} must be {dt}, got {t.dtype}")
-            if not t.is_cuda or t.device.index != self.device:
-                raise ValueError(f"{name} must be on cuda:{self.device}")
-            if not t.is_contiguous():
-                raise ValueError(f"{name} must be contiguous")
+        _check_tensors(self.device, (("q", q, torch.bfloat16), ("k_cache", k_cache, torch.bfloat16),
+                                     ("v_cache", v_cache, torch.bfloat16), ("seq_offsets", seq_offsets, torch.int32),
+                                     ("seq_lens", seq_lens, torch.int32), ("q_starts", q_starts, torch.int32),
+                                     ("q_lens", q_lens, torch.int32), ("out", out, self.out_dtype)))
         b = seq_lens.shape[0]
         if q.dim() != 3 or q.shape[1:] != (d.num_q_heads, d.head_dim) or out.shape != q.shape:
             raise ValueError(f"q/out must be [rows, {d.num_q_heads}, {d.head_dim}]")
@@ -267,9 +265,7 @@ class DecodeAttention:
             raise ValueError(f"k_cache/v_cache must be [rows, {d.num_kv_heads}, {d.head_dim}]")
         if seq_offsets.shape != (b,) or q_starts.shape != (b,) or q_lens.shape != (b,):
             raise ValueError(f"seq_offsets, seq_lens, q_starts, q_lens must all be [{b}]")
-        if stream is None:
-            stream = torch.cuda.current_stream()
-        sp = stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream)
+        sp = _stream_ptr(stream)
         rc = self.lib.ctx_prefill_attn_run(self.handle, q.data_ptr(), k_cache.data_ptr(), v_cache.data_ptr(),
                                            seq_offsets.data_ptr(), seq_lens.data_ptr(), q_starts.data_ptr(),
                                            q_lens.data_ptr(), b, int(max_q_len), float(scale), out.data_ptr(), sp)
@@ -348,9 +344,7 @@ def opd_loss(logits, tokens, old_logp, teacher_logp, mask, seq_starts, params: O
         elif g.dtype != torch.bfloat16 or g.dim() != 2 or g.shape[0] != n or g.stride(1) != 1:
             raise ValueError("out['grad_logits'] must be bf16 [N, >= vocab] with unit column stride")
         res["grad_logits"] = g if out.get("grad_logits") is not None else g[:, :vocab]
-    if stream is None:
-        stream = torch.cuda.current_stream(dev)
-    sp = stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream)
+    sp = _stream_ptr(stream, dev)
     rc = lib.ctx_opd_loss_run(logits.data_ptr(), logits.stride(0), vocab, tokens.data_ptr(), old_logp.data_ptr(),
                               teacher_logp.data_ptr(), mask.data_ptr(), seq_starts.data_ptr(),
                               seq_starts.shape[0] - 1, n, ctypes.byref(params), res["token_logp"].data_ptr(),
