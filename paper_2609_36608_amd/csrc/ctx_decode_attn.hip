@@ -8,8 +8,9 @@
 // Design (flash-decoding split-K, register resident):
 //   * Work split.  The batch's tokens, flattened sequence after sequence, are
 //     cut into equal ranges, one wave per (range, KV head), sized so the
-//     whole grid is resident at once; a workgroup holds the waves of up to 4
-//     KV heads of one range, each with its own LDS tiles.  Every wave derives its ranges from seq_lens on the device,
+//     whole grid is resident at once; a workgroup holds the waves of up to 8
+//     KV heads of one range (whole 2 KiB token rows for Hkv = 8), each with
+//     its own LDS tiles.  Every wave derives its ranges from seq_lens on the device,
 //     so no host sync is needed and the call is graph-capturable.  A range
 //     that holds a whole sequence writes that sequence's output directly;
 //     otherwise each piece writes an fp32 partial (m, l, o) to the workspace
@@ -50,7 +51,7 @@ constexpr int kBlock = 16;        // tokens per MFMA block
 constexpr int kMaxGroup = 16;     // query heads per KV head (MFMA N dimension)
 constexpr int kMinRange = 64;     // smallest balanced range, tokens
 constexpr int kMergeWaves = 4;
-constexpr int kWgWaves = 4;  // most waves (KV heads of one range) per split workgroup
+constexpr int kWgWaves = 8;  // most waves (KV heads of one range) per split workgroup
 constexpr int kTileBytes = 2 * kBlock * kHeadDim * 2;  // one wave's K and V tiles in LDS
 #ifndef CTX_WAVES_PER_EU
 #define CTX_WAVES_PER_EU 3
@@ -590,8 +591,8 @@ int ctx_decode_attn_create(const ctx_decode_attn_desc* desc, ctx_decode_attn** o
   int cus = 0;
   e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
   if (e != hipSuccess) return hip_fail(e, "hipDeviceGetAttribute");
-  // Workgroups hold the KV heads of one range: 4, 2 or 1 of them (a divisor of
-  // Hkv).  Resident waves per CU: the smaller of the two layouts' kernels.
+  // Workgroups hold the KV heads of one range: 8, 4, 2 or 1 of them (a divisor
+  // of Hkv).  Resident waves per CU: the smaller of the two layouts' kernels.
   int wgw = kWgWaves;
   while (d.num_kv_heads % wgw != 0) wgw >>= 1;
   const void* kernels[2] = {
