@@ -22,7 +22,7 @@ struct ctx_decode_attn {
   ctx_decode_attn_desc desc;
   int device;
   int num_cus;
-  int32_t ranges_auto;  // ranges of the balanced split
+  int32_t ranges_auto[2];  // ranges of the balanced split: contiguous, paged layout
   int64_t max_ranges;   // most ranges any run call can use
   int32_t split_wgw;    // waves (KV heads of one range) per split workgroup
   float* o_ws;

@@ -53,9 +53,12 @@ constexpr int kMinRange = 64;     // smallest balanced range, tokens
 constexpr int kMergeWaves = 4;
 constexpr int kWgWaves = 8;  // most waves (KV heads of one range) per split workgroup
 constexpr int kTileBytes = 2 * kBlock * kHeadDim * 2;  // one wave's K and V tiles in LDS
-#ifndef CTX_WAVES_PER_EU
-#define CTX_WAVES_PER_EU 3
-#endif
+// Waves per SIMD the split kernel is compiled for: 3 for contiguous caches
+// (167 VGPRs); the paged kernel's page bookkeeping needs more registers and
+// spills at 3, so it is compiled for 2.  An 8-wave workgroup (Hkv = 8) is one
+// workgroup per CU either way.
+constexpr int kWavesPerEu = 3;
+constexpr int kPagedWavesPerEu = 2;
 
 struct Plan {
   int32_t num_seqs;
@@ -228,7 +231,7 @@ __device__ __forceinline__ void attend_block(const u32x4 (&kr)[4], const u32x4 (
 // ------------------------------------------------------------ split kernel
 
 template <typename OutT, bool kPaged>
-__global__ __launch_bounds__(64 * kWgWaves) __attribute__((amdgpu_waves_per_eu(CTX_WAVES_PER_EU))) void decode_split_kernel(
+__global__ __launch_bounds__(64 * kWgWaves) __attribute__((amdgpu_waves_per_eu(kPaged ? kPagedWavesPerEu : kWavesPerEu))) void decode_split_kernel(
     const uint16_t* __restrict__ q, const uint16_t* __restrict__ kc,
     const uint16_t* __restrict__ vc, const int32_t* __restrict__ offs,
     const int32_t* __restrict__ lens, Plan p, Paged pg, float* __restrict__ o_ws,
@@ -325,12 +328,49 @@ __global__ __launch_bounds__(64 * kWgWaves) __attribute__((amdgpu_waves_per_eu(C
       // the appended token (paged, with k_new): the last token of a sequence
       const bool append = kPaged && pg.k_new != nullptr && s1 == seq_len;
 
+      const int voff = (lane >> 4) * row_bytes + (lane & 15) * 16;
+      const int ld_tok = lane >> 4;
       // Coalesced loads: 16 lanes cover one token's 256-byte head slice, four
       // tokens per instruction.  The block goes through a wave-private LDS
       // tile (16-byte chunks XOR-swizzled by token, conflict-free both ways)
-      // and is read back in the MFMA operand layout.
-      const int voff = (lane >> 4) * row_bytes + (lane & 15) * 16;
-      const int ld_tok = lane >> 4;
+      // and is read back in the MFMA operand layout.  The next block's loads
+      // are issued as soon as the current block is in LDS, so they are in
+      // flight during its math.
+      u32x4 pk[4], pv[4];
+      // Issue the loads of the block at segment token t into pk, pv and return
+      // its first cache row.  Past the segment end the range is empty: the
+      // loads return zeros and touch no memory.
+      auto issue = [&](int t) __attribute__((always_inline)) -> size_t {
+        const int v = len - t < kBlock ? len - t : kBlock;
+        size_t row = 0;
+        if (v > 0) {
+          if (kPaged) {
+            const int64_t tok = s0 + t;
+            int pj = (int)(tok / pg.page_tokens) - page_base;
+            if (pj >= 64) {  // the segment ran past the pages held in registers
+              page_base += 64;
+              pj -= 64;
+              const int used = (int)((seq_len + pg.page_tokens - 1) / pg.page_tokens);
+              const int j = page_base + lane;
+              page_lane = j < used && j < pg.max_pages ? pg.block_tables[(size_t)b * pg.max_pages + j] : 0;
+            }
+            const int page = __builtin_amdgcn_readlane(page_lane, pj);
+            row = (size_t)page * pg.page_tokens + (size_t)(tok % pg.page_tokens);
+          } else {
+            row = (size_t)t;
+          }
+        }
+        const uint32_t bytes = v > 0 ? (uint32_t)(v * row_bytes) : 0u;
+        const __amdgpu_buffer_rsrc_t rk = make_rsrc(kseg + row * row_elems, bytes);
+        const __amdgpu_buffer_rsrc_t rv = make_rsrc(vseg + row * row_elems, bytes);
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          pk[u] = buf_load16(rk, voff, 4 * u * row_bytes);
+          pv[u] = buf_load16(rv, voff, 4 * u * row_bytes);
+        }
+        return row;
+      };
+      size_t blk_row = issue(0);
       for (int t = 0; t < len; t += kBlock) {
         const int valid = len - t < kBlock ? len - t : kBlock;
         {
@@ -344,31 +384,6 @@ __global__ __launch_bounds__(64 * kWgWaves) __attribute__((amdgpu_waves_per_eu(C
           else if (done < 2 * quarter) __builtin_amdgcn_s_setprio(2);
           else if (done < 3 * quarter) __builtin_amdgcn_s_setprio(1);
           else __builtin_amdgcn_s_setprio(0);
-        }
-        size_t blk_row;  // first cache row of the block
-        if (kPaged) {
-          const int64_t tok = s0 + t;
-          int pj = (int)(tok / pg.page_tokens) - page_base;
-          if (pj >= 64) {  // the segment ran past the pages held in registers
-            page_base += 64;
-            pj -= 64;
-            const int used = (int)((seq_len + pg.page_tokens - 1) / pg.page_tokens);
-            const int j = page_base + lane;
-            page_lane = j < used && j < pg.max_pages ? pg.block_tables[(size_t)b * pg.max_pages + j] : 0;
-          }
-          const int page = __builtin_amdgcn_readlane(page_lane, pj);
-          blk_row = (size_t)page * pg.page_tokens + (size_t)(tok % pg.page_tokens);
-        } else {
-          blk_row = (size_t)t;
-        }
-        const uint32_t bytes = (uint32_t)(valid * row_bytes);
-        const __amdgpu_buffer_rsrc_t rk = make_rsrc(kseg + blk_row * row_elems, bytes);
-        const __amdgpu_buffer_rsrc_t rv = make_rsrc(vseg + blk_row * row_elems, bytes);
-        u32x4 pk[4], pv[4];
-#pragma unroll
-        for (int u = 0; u < 4; ++u) {
-          pk[u] = buf_load16(rk, voff, 4 * u * row_bytes);
-          pv[u] = buf_load16(rv, voff, 4 * u * row_bytes);
         }
         __builtin_amdgcn_wave_barrier();  // keep the previous block's LDS reads before these writes
 #pragma unroll
@@ -394,6 +409,7 @@ __global__ __launch_bounds__(64 * kWgWaves) __attribute__((amdgpu_waves_per_eu(C
             *reinterpret_cast<u32x4*>(pg.v_cache + dst) = nv;
           }
         }
+        const size_t next_row = issue(t + kBlock);
         __builtin_amdgcn_wave_barrier();
         u32x4 kr[4], vr[4];
 #pragma unroll
@@ -403,6 +419,7 @@ __global__ __launch_bounds__(64 * kWgWaves) __attribute__((amdgpu_waves_per_eu(C
           vr[kk] = *reinterpret_cast<const u32x4*>(&lds_v[slot]);
         }
         attend_block(kr, vr, qb, sel, valid, c, p.scale_log2, st, o);
+        blk_row = next_row;
       }
 
       float l_tot = st.l + __shfl_xor(st.l, 16);
@@ -592,7 +609,8 @@ int ctx_decode_attn_create(const ctx_decode_attn_desc* desc, ctx_decode_attn** o
   e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
   if (e != hipSuccess) return hip_fail(e, "hipDeviceGetAttribute");
   // Workgroups hold the KV heads of one range: 8, 4, 2 or 1 of them (a divisor
-  // of Hkv).  Resident waves per CU: the smaller of the two layouts' kernels.
+  // of Hkv).  Each layout's kernel gets the ranges that keep one wave per
+  // (range, KV head) resident.
   int wgw = kWgWaves;
   while (d.num_kv_heads % wgw != 0) wgw >>= 1;
   const void* kernels[2] = {
@@ -600,20 +618,17 @@ int ctx_decode_attn_create(const ctx_decode_attn_desc* desc, ctx_decode_attn** o
                                    : reinterpret_cast<const void*>(&decode_split_kernel<uint16_t, false>),
       d.out_dtype == CTX_DTYPE_F32 ? reinterpret_cast<const void*>(&decode_split_kernel<float, true>)
                                    : reinterpret_cast<const void*>(&decode_split_kernel<uint16_t, true>)};
-  int per_cu = 1 << 30;
-  for (const void* kern : kernels) {
+  int64_t ranges_auto[2];
+  for (int layout = 0; layout < 2; ++layout) {
     int n = 0;
-    e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, kern, 64 * wgw, (size_t)wgw * kTileBytes);
+    e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, kernels[layout], 64 * wgw, (size_t)wgw * kTileBytes);
     if (e != hipSuccess) return hip_fail(e, "hipOccupancyMaxActiveBlocksPerMultiprocessor");
-    n *= wgw;  // waves
-    if (n < per_cu) per_cu = n;
+    const int64_t per_cu = n < 1 ? 1 : (int64_t)n * wgw;  // resident waves per CU
+    // ranges in whole multiples of the XCD count
+    ranges_auto[layout] = (int64_t)cus * per_cu / d.num_kv_heads / kXcds * kXcds;
+    if (ranges_auto[layout] < kXcds) ranges_auto[layout] = kXcds;
   }
-  if (per_cu < 1) per_cu = 1;
-
-  // one resident wave per (range, KV head); ranges in whole multiples of the XCD count
-  int64_t ranges_auto = (int64_t)cus * per_cu / d.num_kv_heads / kXcds * kXcds;
-  if (ranges_auto < kXcds) ranges_auto = kXcds;
-  int64_t max_ranges = ranges_auto;
+  int64_t max_ranges = ranges_auto[0] > ranges_auto[1] ? ranges_auto[0] : ranges_auto[1];
   if (d.split_tokens > 0)
     max_ranges = round_up(((int64_t)d.max_batch * round_up(d.max_seq_len, kBlock) + d.split_tokens - 1) /
                               d.split_tokens, kXcds);
@@ -630,7 +645,8 @@ int ctx_decode_attn_create(const ctx_decode_attn_desc* desc, ctx_decode_attn** o
   h->desc = d;
   h->device = dev;
   h->num_cus = cus;
-  h->ranges_auto = (int32_t)ranges_auto;
+  h->ranges_auto[0] = (int32_t)ranges_auto[0];
+  h->ranges_auto[1] = (int32_t)ranges_auto[1];
   h->max_ranges = max_ranges;
   h->split_wgw = wgw;
   e = hipMalloc(reinterpret_cast<void**>(&h->o_ws), o_bytes);
@@ -662,7 +678,7 @@ int launch(ctx_decode_attn* h, const void* q, const void* k, const void* v, cons
   p.num_ranges = d.split_tokens > 0
                      ? (int32_t)round_up(((int64_t)num_seqs * round_up(d.max_seq_len, kPaged ? kBlock : 1) +
                                           d.split_tokens - 1) / d.split_tokens, kXcds)
-                     : h->ranges_auto;
+                     : h->ranges_auto[kPaged ? 1 : 0];
   p.pad = kPaged ? kBlock : 1;
   p.scale_log2 = (float)((double)scale * 1.4426950408889634);
 
