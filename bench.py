@@ -206,23 +206,29 @@ def bench_prefill(args) -> int:
     stream = torch.cuda.current_stream()
     max_q = int(nq.max())
 
-    def step() -> None:
+    def step(split_p: bool) -> None:
         for layer in range(w.layers):
             attn.prefill(q, ks[layer % n_buf], vs[layer % n_buf], t_offs, t_lens, t_qs, t_nq, max_q,
-                         w.scale, out, stream=stream)
+                         w.scale, out, stream=stream, split_p=split_p)
 
-    for _ in range(args.warmup):
-        step()
-    torch.cuda.synchronize()
-    start = torch.cuda.Event(enable_timing=True)
-    stop = torch.cuda.Event(enable_timing=True)
-    start.record(stream)
-    for _ in range(args.steps):
-        step()
-    stop.record(stream)
-    stop.synchronize()
-    torch.cuda.synchronize()
-    elapsed_s = start.elapsed_time(stop) / 1e3
+    def time_mode(split_p: bool) -> float:
+        for _ in range(args.warmup):
+            step(split_p)
+        torch.cuda.synchronize()
+        start = torch.cuda.Event(enable_timing=True)
+        stop = torch.cuda.Event(enable_timing=True)
+        start.record(stream)
+        for _ in range(args.steps):
+            step(split_p)
+        stop.record(stream)
+        stop.synchronize()
+        torch.cuda.synchronize()
+        return start.elapsed_time(stop) / 1e3
+
+    # the default precision (bf16 softmax weights) gives `value`; the two-term
+    # weights (CTX_PREFILL_SPLIT_P) are timed beside it
+    split_s = time_mode(True) if args.prefill_p in ("both", "split") else None
+    elapsed_s = time_mode(False) if args.prefill_p in ("both", "bf16") else split_s
     calls = args.steps * w.layers
     flops = prefill_flops(lens, nq, w)
     if args.calibrate_copy_gib > 0:
@@ -266,13 +272,21 @@ def bench_prefill(args) -> int:
             "unit": "TFLOP/s",
             "frac": round(flops / (elapsed_s / calls) / 1e12 / MFMA_BF16_PEAK_TFLOPS, 4),
             "traffic": profiled_traffic(w.name, "prefill_kernel"),
-            "kernel": "prefill_kernel (one ctx_prefill_attn_run call per layer)",
+            "kernel": ("prefill_kernel (one ctx_prefill_attn_run call per layer, "
+                       + ("two-term softmax weights)" if args.prefill_p == "split" else "bf16 softmax weights)")),
             "flops_per_launch": flops,
             "kv_bytes_per_launch": kv_bytes,
             "avg_launch_us": round(elapsed_s / calls * 1e6, 3),
         },
         "setup_s": round(setup_s, 1),
     }
+    if split_s is not None and args.prefill_p == "both":
+        result["split_p"] = {
+            "value": round(flops * calls / split_s / 1e12, 2),
+            "ms_per_step": round(split_s * 1e3 / args.steps, 4),
+            "avg_launch_us": round(split_s / calls * 1e6, 3),
+            "frac": round(flops * calls / split_s / 1e12 / MFMA_BF16_PEAK_TFLOPS, 4),
+        }
     if not args.no_cpu_baseline:
         threads = len(os.sched_getaffinity(0))
         result["cpu_baseline"] = prefill_cpu_baseline(w, lens, nq, args.cpu_seconds, threads)
@@ -596,6 +610,9 @@ def main() -> int:
     ap.add_argument("--prefill", action="store_true",
                     help="time the causal prefill of the appended reference observation instead "
                          "(act_first_burst)")
+    ap.add_argument("--prefill-p", choices=("both", "bf16", "split"), default="both",
+                    help="with --prefill: softmax-weight precision(s) to time; `value` is the bf16 "
+                         "weights (the default of ctx_prefill_attn_run) unless only split is timed")
     ap.add_argument("--opd", action="store_true",
                     help="time the fused OPD token loss + logits gradient instead (64 responses, Qwen3 vocabulary)")
     ap.add_argument("--sim", action="store_true",

@@ -164,15 +164,24 @@ int ctx_decode_attn_run_paged(ctx_decode_attn* handle, const void* q, void* k_pa
  *   q_starts, q_lens  int32 [num_seqs]; 0 <= q_lens[b] <= seq_lens[b] and
  *                q_lens[b] <= max_q_len (device contract: undefined otherwise)
  *   max_q_len    host bound on q_lens (sizes the grid)
+ *   flags        0 or CTX_PREFILL_SPLIT_P.  With 0 the softmax weights enter the
+ *                P.V product rounded to bf16 (nearest even), and each row is
+ *                normalised by the sum of the rounded weights, so it stays a convex
+ *                combination of V rows (weights within 2^-9 relative of exact; a few
+ *                1e-3 absolute on N(0,1) data).  CTX_PREFILL_SPLIT_P carries the
+ *                weights as two bf16 terms (16 significant bits; about 1e-6
+ *                absolute) at half again the matrix-core work.
  *   out          [total_q, Hq, D] of desc.out_dtype; rows of no sequence are untouched
  * Needs a group size Hq / Hkv dividing 16 (UNSUPPORTED otherwise).  No
  * workspace, no allocation, no host sync; deterministic.
- * Errors: INVALID_ARG, UNSUPPORTED, CAPACITY, ALIGNMENT, HIP.
+ * Errors: INVALID_ARG (also for unknown flag bits), UNSUPPORTED, CAPACITY,
+ * ALIGNMENT, HIP.
  */
+#define CTX_PREFILL_SPLIT_P 1u
 int ctx_prefill_attn_run(ctx_decode_attn* handle, const void* q, const void* k_cache, const void* v_cache,
                          const int32_t* seq_offsets, const int32_t* seq_lens, const int32_t* q_starts,
                          const int32_t* q_lens, int32_t num_seqs, int32_t max_q_len, float scale,
-                         void* out, void* stream);
+                         uint32_t flags, void* out, void* stream);
 
 /* Wait for the handle's device, free the workspace and the handle.  NULL is a no-op. */
 int ctx_decode_attn_destroy(ctx_decode_attn* handle);

@@ -22,6 +22,8 @@ CTX_ERR_OOM = -6
 CTX_DTYPE_BF16 = 0
 CTX_DTYPE_F32 = 1
 
+CTX_PREFILL_SPLIT_P = 1  # ctx_prefill_attn_run flag: softmax weights as two bf16 terms
+
 # every function the C header declares
 EXPORTS = (
     "ctx_decode_attn_create",
@@ -107,7 +109,8 @@ def load_library(path: str | None = None):
     lib.ctx_decode_attn_run.restype = ctypes.c_int
     lib.ctx_decode_attn_run_paged.argtypes = [vp, vp, vp, vp, vp, i32, vp, i32, vp, vp, ctypes.c_float, vp, vp]
     lib.ctx_decode_attn_run_paged.restype = ctypes.c_int
-    lib.ctx_prefill_attn_run.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp, i32, i32, ctypes.c_float, vp, vp]
+    lib.ctx_prefill_attn_run.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp, i32, i32, ctypes.c_float, ctypes.c_uint32,
+                                         vp, vp]
     lib.ctx_prefill_attn_run.restype = ctypes.c_int
     lib.ctx_opd_loss_run.argtypes = [vp, ctypes.c_int64, i32, vp, vp, vp, vp, vp, i32, i32,
                                      ctypes.POINTER(OpdParams), vp, vp, vp, vp, vp, ctypes.c_int64, vp]
@@ -246,9 +249,11 @@ class DecodeAttention:
         return out
 
     def prefill(self, q, k_cache, v_cache, seq_offsets, seq_lens, q_starts, q_lens, max_q_len: int,
-                scale: float, out, stream=None):
+                scale: float, out, stream=None, split_p: bool = False):
         """Causal prefill: q / out [total_q, Hq, D]; sequence b's q_lens[b] queries
-        (rows q_starts[b] ..) are the last q_lens[b] of its seq_lens[b] cached rows."""
+        (rows q_starts[b] ..) are the last q_lens[b] of its seq_lens[b] cached rows.
+        split_p: carry the softmax weights as two bf16 terms (CTX_PREFILL_SPLIT_P)
+        instead of one."""
         import torch
 
         if self.handle is None:
@@ -268,7 +273,8 @@ class DecodeAttention:
         sp = _stream_ptr(stream)
         rc = self.lib.ctx_prefill_attn_run(self.handle, q.data_ptr(), k_cache.data_ptr(), v_cache.data_ptr(),
                                            seq_offsets.data_ptr(), seq_lens.data_ptr(), q_starts.data_ptr(),
-                                           q_lens.data_ptr(), b, int(max_q_len), float(scale), out.data_ptr(), sp)
+                                           q_lens.data_ptr(), b, int(max_q_len), float(scale),
+                                           CTX_PREFILL_SPLIT_P if split_p else 0, out.data_ptr(), sp)
         if rc != CTX_OK:
             raise error_for(self.lib, rc)
         return out

@@ -9,14 +9,17 @@
 // columns of one (sequence, KV head) and streams 32-token K/V blocks, up to
 // its last query position, through a three-stage LDS tile that all its
 // waves share; the blocks are loaded straight into LDS, two blocks ahead of
-// the math.  Per 16 tokens and 16 columns a wave computes
-//   S^T = K Q^T                 (4 MFMA 16x16x32, K rows straight from LDS)
-//   causal mask, lazy online softmax, P = P_hi + P_lo (two bf16 terms)
-//   O^T += V^T [P_hi | P_lo]^T  (8 MFMA 16x16x32: the hi and lo terms are the
-//                                two halves of the K dimension, V^T repeated)
+// the math.  Per 32 tokens and 16 columns a wave computes
+//   S^T = K Q^T                 (8 MFMA 16x16x32, K rows straight from LDS)
+//   causal mask, lazy online softmax
+//   O^T += V^T P^T              (8 MFMA 16x16x32 per bf16 term of P)
 // where the V^T operand comes from the row-major LDS tile through the LDS
 // transpose read, whose 4 values per lane are tokens 4c..4c+3 of one
-// dimension -- the rows the S^T tile gives each lane.
+// dimension -- the rows the S^T tile gives each lane.  P enters the product
+// either as one bf16 term (rounded to nearest even; the row sum is taken over
+// the rounded weights, so each output row stays a convex combination of V
+// rows) or, with CTX_PREFILL_SPLIT_P, as P_hi + P_lo (16 significant bits, a
+// second set of 8 MFMAs).
 
 #include <hip/hip_runtime.h>
 
@@ -74,7 +77,7 @@ __device__ __forceinline__ void split_bf16x2(float a, float b, uint32_t* hi, uin
   *lo = pack_bf16x2(a - __uint_as_float(ua & 0xffff0000u), b - __uint_as_float(ub & 0xffff0000u));
 }
 
-template <typename OutT>
+template <typename OutT, bool kSplitP>
 __global__ __launch_bounds__(64 * kPrefillWaves) __attribute__((amdgpu_waves_per_eu(2))) void prefill_kernel(
     const uint16_t* __restrict__ q, const uint16_t* __restrict__ kc, const uint16_t* __restrict__ vc,
     const int32_t* __restrict__ offs, const int32_t* __restrict__ lens,
@@ -262,13 +265,24 @@ __global__ __launch_bounds__(64 * kPrefillWaves) __attribute__((amdgpu_waves_per
 #pragma unroll
             for (int i = 0; i < 4; ++i) pr[4 * h + i] = fast_exp2(fmaf(sc[ct][h][i], cs, -st[ct].m));
         }
-        st[ct].l += ((pr[0] + pr[1]) + (pr[2] + pr[3])) + ((pr[4] + pr[5]) + (pr[6] + pr[7]));
+        if (kSplitP) {
+          st[ct].l += ((pr[0] + pr[1]) + (pr[2] + pr[3])) + ((pr[4] + pr[5]) + (pr[6] + pr[7]));
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          uint32_t hw, lw;
-          split_bf16x2(pr[2 * j], pr[2 * j + 1], &hw, &lw);
-          phi[ct][j] = hw;
-          plo[ct][j] = lw;
+          for (int j = 0; j < 4; ++j) {
+            uint32_t hw, lw;
+            split_bf16x2(pr[2 * j], pr[2 * j + 1], &hw, &lw);
+            phi[ct][j] = hw;
+            plo[ct][j] = lw;
+          }
+        } else {
+          // one bf16 term; the row sum adds the rounded weights the product uses
+          float rs[4];
+#pragma unroll
+          for (int j = 0; j < 4; ++j) {
+            phi[ct][j] = pack_bf16x2(pr[2 * j], pr[2 * j + 1]);
+            rs[j] = __uint_as_float(phi[ct][j] << 16) + __uint_as_float(phi[ct][j] & 0xffff0000u);
+          }
+          st[ct].l += (rs[0] + rs[1]) + (rs[2] + rs[3]);
         }
       }
       // O^T += V^T P^T: the K dimension holds tokens 4c..4c+3 of both halves.
@@ -284,9 +298,11 @@ __global__ __launch_bounds__(64 * kPrefillWaves) __attribute__((amdgpu_waves_per
 #pragma unroll
         for (int ct = 0; ct < kPrefillTiles; ++ct)
           o[ct][nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(va, as_bf16x8(phi[ct]), o[ct][nb], 0, 0, 0);
+        if (kSplitP) {
 #pragma unroll
-        for (int ct = 0; ct < kPrefillTiles; ++ct)
-          o[ct][nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(va, as_bf16x8(plo[ct]), o[ct][nb], 0, 0, 0);
+          for (int ct = 0; ct < kPrefillTiles; ++ct)
+            o[ct][nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(va, as_bf16x8(plo[ct]), o[ct][nb], 0, 0, 0);
+        }
       }
       __builtin_amdgcn_s_setprio(0);
     }
@@ -320,7 +336,7 @@ __global__ __launch_bounds__(64 * kPrefillWaves) __attribute__((amdgpu_waves_per
 extern "C" int ctx_prefill_attn_run(ctx_decode_attn* h, const void* q, const void* k_cache, const void* v_cache,
                          const int32_t* seq_offsets, const int32_t* seq_lens, const int32_t* q_starts,
                          const int32_t* q_lens, int32_t num_seqs, int32_t max_q_len, float scale,
-                         void* out, void* stream) {
+                         uint32_t flags, void* out, void* stream) {
   int rc = check_common(h, num_seqs, scale);
   if (rc != CTX_OK) return rc;
   const ctx_decode_attn_desc& d = h->desc;
@@ -328,6 +344,7 @@ extern "C" int ctx_prefill_attn_run(ctx_decode_attn* h, const void* q, const voi
   if (16 % g != 0)
     return fail(CTX_ERR_UNSUPPORTED, "prefill needs a group size dividing 16 (got %d)", g);
   if (max_q_len < 0) return fail(CTX_ERR_INVALID_ARG, "max_q_len %d < 0", max_q_len);
+  if ((flags & ~CTX_PREFILL_SPLIT_P) != 0) return fail(CTX_ERR_INVALID_ARG, "unknown prefill flags 0x%x", flags);
   if (num_seqs == 0 || max_q_len == 0) return CTX_OK;
   if (q == nullptr || k_cache == nullptr || v_cache == nullptr || seq_offsets == nullptr ||
       seq_lens == nullptr || q_starts == nullptr || q_lens == nullptr || out == nullptr)
@@ -349,12 +366,25 @@ extern "C" int ctx_prefill_attn_run(ctx_decode_attn* h, const void* q, const voi
   const uint16_t* qp = static_cast<const uint16_t*>(q);
   const uint16_t* kp = static_cast<const uint16_t*>(k_cache);
   const uint16_t* vp = static_cast<const uint16_t*>(v_cache);
-  if (d.out_dtype == CTX_DTYPE_F32)
-    hipLaunchKernelGGL(prefill_kernel<float>, dim3((unsigned)blocks), dim3(64 * kPrefillWaves), 0, s, qp,
-                       kp, vp, seq_offsets, seq_lens, q_starts, q_lens, pp, static_cast<float*>(out));
-  else
-    hipLaunchKernelGGL(prefill_kernel<uint16_t>, dim3((unsigned)blocks), dim3(64 * kPrefillWaves), 0, s,
-                       qp, kp, vp, seq_offsets, seq_lens, q_starts, q_lens, pp, static_cast<uint16_t*>(out));
+  const dim3 grid((unsigned)blocks), block(64 * kPrefillWaves);
+  const bool split_p = (flags & CTX_PREFILL_SPLIT_P) != 0;
+  if (d.out_dtype == CTX_DTYPE_F32) {
+    float* op = static_cast<float*>(out);
+    if (split_p)
+      hipLaunchKernelGGL((prefill_kernel<float, true>), grid, block, 0, s, qp, kp, vp, seq_offsets, seq_lens,
+                         q_starts, q_lens, pp, op);
+    else
+      hipLaunchKernelGGL((prefill_kernel<float, false>), grid, block, 0, s, qp, kp, vp, seq_offsets, seq_lens,
+                         q_starts, q_lens, pp, op);
+  } else {
+    uint16_t* op = static_cast<uint16_t*>(out);
+    if (split_p)
+      hipLaunchKernelGGL((prefill_kernel<uint16_t, true>), grid, block, 0, s, qp, kp, vp, seq_offsets, seq_lens,
+                         q_starts, q_lens, pp, op);
+    else
+      hipLaunchKernelGGL((prefill_kernel<uint16_t, false>), grid, block, 0, s, qp, kp, vp, seq_offsets,
+                         seq_lens, q_starts, q_lens, pp, op);
+  }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return hip_fail(e, "kernel launch");
   return CTX_OK;

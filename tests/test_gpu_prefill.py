@@ -1,5 +1,10 @@
 """Causal prefill of the newest tokens (the appended reference observation)
-against the cache, through ctx_prefill_attn_run, against the CPU oracle."""
+against the cache, through ctx_prefill_attn_run, against the CPU oracle.
+
+Both precisions of the P.V product are covered: the default (softmax weights
+rounded to bf16, rows normalised by the sum of the rounded weights) against
+the parity gate, and CTX_PREFILL_SPLIT_P (two bf16 terms) also against the
+fp32-rounding bound."""
 import numpy as np
 import pytest
 import torch
@@ -42,50 +47,85 @@ def prefill_case(seed, hq, hkv, batch, hist, new, peaky=False):
     return w, lay, lens, nq, q_starts, q, k, v
 
 
-def run_prefill(w, lay, lens, nq, q_starts, q, k, v, out_dtype=torch.float32):
+def run_prefill(w, lay, lens, nq, q_starts, q, k, v, out_dtype=torch.float32, split_p=False):
     total_q = q.shape[0]
     with DecodeAttention(w.num_q_heads, w.num_kv_heads, len(lens), int(lens.max()), out_dtype=out_dtype) as attn:
         out = torch.full((total_q, w.num_q_heads, 128), -555.0, dtype=out_dtype, device=dev())
         attn.prefill(up_bf16(q), up_bf16(k), up_bf16(v), up_i32(lay.offsets), up_i32(lens), up_i32(q_starts),
-                     up_i32(nq), int(nq.max()), w.scale, out)
+                     up_i32(nq), int(nq.max()), w.scale, out, split_p=split_p)
         torch.cuda.synchronize()
     return out.float().cpu().numpy()
 
 
+MODES = [pytest.param(False, id="bf16p"), pytest.param(True, id="splitp")]
+
+
+@pytest.mark.parametrize("split_p", MODES)
 @pytest.mark.parametrize("hq,hkv", [(32, 8), (16, 8), (16, 16), (16, 1), (64, 8)])
-def test_prefill_parity(hq, hkv):
+def test_prefill_parity(hq, hkv, split_p):
     w, lay, lens, nq, qs, q, k, v = prefill_case(hq * 3 + hkv, hq, hkv, batch=7, hist=(0, 500), new=(1, 140))
     nq[0], nq[1] = 1, 128 // (hq // hkv) + 1  # decode-like and one past a workgroup tile
     lens[1] = max(lens[1], nq[1])
     ref = oracle.prefill_attn(q, k, v, lay.offsets, lens, qs, nq, w.scale)
-    got = run_prefill(w, lay, lens, nq, qs, q, k, v)
+    got = run_prefill(w, lay, lens, nq, qs, q, k, v, split_p=split_p)
     rows = np.zeros(q.shape[0], bool)
     for b in range(len(lens)):
         rows[qs[b]:qs[b] + nq[b]] = True
-    assert_parity(got[rows], ref[rows], f"prefill {hq}/{hkv}")
+    assert_parity(got[rows], ref[rows], f"prefill {hq}/{hkv} split_p={split_p}", tight=split_p)
     assert (got[~rows] == -555.0).all(), "wrote a row of no sequence"
 
 
-def test_prefill_fresh_prompt_and_peaky_keys():
+@pytest.mark.parametrize("split_p", MODES)
+def test_prefill_fresh_prompt_and_peaky_keys(split_p):
     """No history (the whole sequence is new: query 0 sees only itself) and
     peaky keys, as in the act-first burst."""
     w, lay, lens, nq, qs, q, k, v = prefill_case(7, 32, 8, batch=5, hist=(0, 0), new=(1, 300), peaky=True)
     ref = oracle.prefill_attn(q, k, v, lay.offsets, lens, qs, nq, w.scale)
-    got = run_prefill(w, lay, lens, nq, qs, q, k, v)
+    got = run_prefill(w, lay, lens, nq, qs, q, k, v, split_p=split_p)
     rows = np.concatenate([np.arange(qs[b], qs[b] + nq[b]) for b in range(5)])
-    assert_parity(got[rows], ref[rows], "fresh prompt")
+    assert_parity(got[rows], ref[rows], f"fresh prompt split_p={split_p}", tight=split_p)
+
+
+@pytest.mark.parametrize("split_p", MODES)
+def test_prefill_constant_v(split_p):
+    """V rows all equal: every output row is that row, to fp32 rounding, in both
+    modes.  In the default mode this holds only because each row is normalised
+    by the sum of the rounded weights that the P.V product uses (normalising by
+    the unrounded sum would be off by up to 2^-9 relative)."""
+    w, lay, lens, nq, qs, q, k, v = prefill_case(23, 32, 8, batch=5, hist=(0, 700), new=(1, 200), peaky=True)
+    row = wl.f32_to_bf16_bits(np.random.default_rng(5).standard_normal((8, 128)).astype(np.float32) * 3)
+    used = np.zeros(v.shape[0], bool)
+    for b in range(5):
+        used[lay.offsets[b]:lay.offsets[b] + lens[b]] = True
+    v = v.copy()
+    v[used] = row[None]
+    got = run_prefill(w, lay, lens, nq, qs, q, k, v, split_p=split_p)
+    want = np.repeat(wl.bf16_bits_to_f32(row), 4, axis=0)  # query head h reads KV head h // 4
+    rows = np.concatenate([np.arange(qs[b], qs[b] + nq[b]) for b in range(5)])
+    err = np.abs(got[rows] - want[None]).max()
+    cmax = float(np.abs(want).max())
+    print(f"constant V split_p={split_p}: max-abs {err:.3e}, max |V| {cmax:.2f}", flush=True)
+    # two terms carry each weight to within 2^-17 relative; one bf16 term with
+    # the matching normaliser is exact up to fp32 accumulation.  Normalising
+    # the bf16 weights by the unrounded sum would be off by up to 2^-9 |V|.
+    assert err <= (2.0**-14 if split_p else 2.0**-16) * cmax
 
 
 def test_prefill_last_row_equals_decode():
-    """The last new token's prefill row is a decode over the whole sequence."""
+    """The last new token's prefill row is a decode over the whole sequence:
+    equal to the decode kernel's output to fp32 rounding with the two-term
+    weights, and within the parity gate of it with bf16 weights."""
     w, lay, lens, nq, qs, q, k, v = prefill_case(11, 32, 8, batch=6, hist=(50, 900), new=(1, 60))
-    got = run_prefill(w, lay, lens, nq, qs, q, k, v)
     last = qs + nq - 1
     with DecodeAttention(32, 8, 6, int(lens.max())) as attn:
         out = torch.empty((6, 32, 128), dtype=torch.float32, device=dev())
         attn.run(up_bf16(q[last]), up_bf16(k), up_bf16(v), up_i32(lay.offsets), up_i32(lens), w.scale, out)
         torch.cuda.synchronize()
-    np.testing.assert_allclose(got[last], out.cpu().numpy(), rtol=0, atol=2e-5)
+    dec = out.cpu().numpy()
+    got = run_prefill(w, lay, lens, nq, qs, q, k, v, split_p=True)
+    np.testing.assert_allclose(got[last], dec, rtol=0, atol=2e-5)
+    got = run_prefill(w, lay, lens, nq, qs, q, k, v, split_p=False)
+    assert_parity(got[last], dec, "bf16 weights against the decode kernel", tight=False)
 
 
 def test_prefill_full_size_act_first_burst_sampled():
@@ -106,9 +146,11 @@ def test_prefill_full_size_act_first_burst_sampled():
     total_q = int(nq.sum())
     q = rand_bits(rng, (total_q, 32, 128))
     out = torch.empty((total_q, 32, 128), dtype=torch.float32, device=dev())
+    out_split = torch.empty_like(out)
     with DecodeAttention(32, 8, w.batch, int(lens.max())) as attn:
-        attn.prefill(up_bf16(q), k, v, up_i32(lay.offsets), up_i32(lens), up_i32(q_starts), up_i32(nq),
-                     int(nq.max()), w.scale, out)
+        args = (up_bf16(q), k, v, up_i32(lay.offsets), up_i32(lens), up_i32(q_starts), up_i32(nq), int(nq.max()), w.scale)
+        attn.prefill(*args, out)
+        attn.prefill(*args, out_split, split_p=True)
         torch.cuda.synchronize()
     seqs = [int(np.argmax(lens)), int(np.argmin(lens)), 3, 100]
     hk, hv, sub_offs, sub_lens, rows = [], [], [], [], []
@@ -124,8 +166,9 @@ def test_prefill_full_size_act_first_burst_sampled():
         base += L
     hk, hv = np.concatenate(hk), np.concatenate(hv)
     ref = oracle.decode_attn(q[rows], hk, hv, np.array(sub_offs), np.array(sub_lens), w.scale)
-    assert_parity(out.cpu().numpy()[rows], ref, f"prefill act-first burst, {len(rows)} sampled rows")
-    assert np.isfinite(out.cpu().numpy()).all()
+    assert_parity(out.cpu().numpy()[rows], ref, f"prefill act-first burst, {len(rows)} sampled rows", tight=False)
+    assert_parity(out_split.cpu().numpy()[rows], ref, "same, two-term weights")
+    assert np.isfinite(out.cpu().numpy()).all() and np.isfinite(out_split.cpu().numpy()).all()
 
 
 def test_prefill_abi():
@@ -137,6 +180,8 @@ def test_prefill_abi():
         o = torch.zeros((2, 24, 128), dtype=torch.float32, device=dev())
         with pytest.raises(CtxError):
             attn.prefill(z, kv, kv, i, i, i, i, 1, 0.1, o)
+        with pytest.raises(CtxError):
+            attn.prefill(z, kv, kv, i, i, i, i, 1, 0.1, o, split_p=True)
     with DecodeAttention(32, 8, 2, 32) as attn:
         h = attn.handle
         z = torch.zeros((2, 32, 128), dtype=torch.bfloat16, device=dev())
@@ -144,25 +189,30 @@ def test_prefill_abi():
         i = torch.zeros(2, dtype=torch.int32, device=dev())
         o = torch.zeros((2, 32, 128), dtype=torch.float32, device=dev())
         P = lambda t, off=0: t.data_ptr() + off  # noqa: E731
-        assert lib.ctx_prefill_attn_run(h, P(z), P(kv), P(kv), P(i), P(i), P(i), P(i), 2, 0, 0.1, P(o), None) == bd.CTX_OK
-        assert lib.ctx_prefill_attn_run(h, P(z), P(kv), P(kv), P(i), P(i), P(i), P(i), 3, 1, 0.1, P(o), None) == bd.CTX_ERR_CAPACITY
-        assert lib.ctx_prefill_attn_run(h, P(z, 2), P(kv), P(kv), P(i), P(i), P(i), P(i), 2, 1, 0.1, P(o), None) == bd.CTX_ERR_ALIGNMENT
-        assert lib.ctx_prefill_attn_run(h, P(z), P(kv), P(kv), P(i), P(i), P(i), None, 2, 1, 0.1, P(o), None) == bd.CTX_ERR_INVALID_ARG
-        assert lib.ctx_prefill_attn_run(h, P(z), P(kv), P(kv), P(i), P(i), P(i), P(i), 2, -1, 0.1, P(o), None) == bd.CTX_ERR_INVALID_ARG
+        run = lib.ctx_prefill_attn_run
+        assert run(h, P(z), P(kv), P(kv), P(i), P(i), P(i), P(i), 2, 0, 0.1, 0, P(o), None) == bd.CTX_OK
+        assert run(h, P(z), P(kv), P(kv), P(i), P(i), P(i), P(i), 2, 1, 0.1, bd.CTX_PREFILL_SPLIT_P, P(o), None) == bd.CTX_OK
+        assert run(h, P(z), P(kv), P(kv), P(i), P(i), P(i), P(i), 2, 1, 0.1, 2, P(o), None) == bd.CTX_ERR_INVALID_ARG
+        assert run(h, P(z), P(kv), P(kv), P(i), P(i), P(i), P(i), 3, 1, 0.1, 0, P(o), None) == bd.CTX_ERR_CAPACITY
+        assert run(h, P(z, 2), P(kv), P(kv), P(i), P(i), P(i), P(i), 2, 1, 0.1, 0, P(o), None) == bd.CTX_ERR_ALIGNMENT
+        assert run(h, P(z), P(kv), P(kv), P(i), P(i), P(i), None, 2, 1, 0.1, 0, P(o), None) == bd.CTX_ERR_INVALID_ARG
+        assert run(h, P(z), P(kv), P(kv), P(i), P(i), P(i), P(i), 2, -1, 0.1, 0, P(o), None) == bd.CTX_ERR_INVALID_ARG
         torch.cuda.synchronize()
 
 
-def test_prefill_bf16_output():
+@pytest.mark.parametrize("split_p", MODES)
+def test_prefill_bf16_output(split_p):
     """bf16 output is the round-to-nearest-even of the fp32 result."""
     w, lay, lens, nq, qs, q, k, v = prefill_case(31, 32, 8, batch=5, hist=(0, 300), new=(1, 100))
-    f32 = run_prefill(w, lay, lens, nq, qs, q, k, v, out_dtype=torch.float32)
-    b16 = run_prefill(w, lay, lens, nq, qs, q, k, v, out_dtype=torch.bfloat16)
+    f32 = run_prefill(w, lay, lens, nq, qs, q, k, v, out_dtype=torch.float32, split_p=split_p)
+    b16 = run_prefill(w, lay, lens, nq, qs, q, k, v, out_dtype=torch.bfloat16, split_p=split_p)
     rows = np.concatenate([np.arange(qs[b], qs[b] + nq[b]) for b in range(5)])
     want = wl.bf16_bits_to_f32(wl.f32_to_bf16_bits(f32[rows].astype(np.float32)))
     np.testing.assert_array_equal(b16[rows], want)
 
 
-def test_prefill_block_boundaries():
+@pytest.mark.parametrize("split_p", MODES)
+def test_prefill_block_boundaries(split_p):
     """Contexts that end on, just before and just after the 32-token K/V
     blocks the workgroup streams (1, 31, 32, 33, 64, 65, 96, 97 tokens), as
     fresh prompts and with a short history: the last blocks' loads, the loads
@@ -178,8 +228,8 @@ def test_prefill_block_boundaries():
     q_starts = np.concatenate([[0], np.cumsum(nq)[:-1]]).astype(np.int32)
     q = rand_bits(rng, (int(nq.sum()), 32, 128))
     ref = oracle.prefill_attn(q, k, v, lay.offsets, lens, q_starts, nq, w.scale)
-    got = run_prefill(w, lay, lens, nq, q_starts, q, k, v)
-    assert_parity(got, ref, "block boundaries")
+    got = run_prefill(w, lay, lens, nq, q_starts, q, k, v, split_p=split_p)
+    assert_parity(got, ref, f"block boundaries split_p={split_p}", tight=split_p)
 
 
 def test_prefill_sequences_without_new_tokens():
@@ -199,5 +249,5 @@ def test_prefill_sequences_without_new_tokens():
     rows = np.zeros(total_q, bool)
     for b in range(6):
         rows[qs[b]:qs[b] + nq[b]] = True
-    assert_parity(got[rows], ref[rows], "with empty sequences")
+    assert_parity(got[rows], ref[rows], "with empty sequences", tight=False)
     assert (got[~rows] == -555.0).all(), "rows of sequences without new tokens were written"
