@@ -28,6 +28,7 @@ from paper_2609_36608_amd import workloads as wl  # noqa: E402
 
 METRIC = "decode-attention HBM GB/s (fraction of 8 TB/s peak) + decode-steps/sec, 1 MI355X"
 HBM_PEAK_GBS = 8000.0
+REPEATS = 20  # individually timed graph replays reported beside the main timed region
 HBM_BUDGET_BYTES = 240 * 2**30  # leave headroom below 288 GB for the rest of the process
 
 
@@ -594,6 +595,17 @@ def bench_sim(args) -> int:
     return 0
 
 
+def device_info(torch, dev) -> dict:
+    """What the measurement ran on, as the runtime reports it."""
+    pr = torch.cuda.get_device_properties(dev)
+    return {
+        "name": pr.name,
+        "arch": getattr(pr, "gcnArchName", ""),
+        "compute_units": pr.multi_processor_count,
+        "hbm_gib": round(pr.total_memory / 2**30, 1),
+    }
+
+
 def main() -> int:
     ap = argparse.ArgumentParser(description=__doc__)
     ap.add_argument("--gpus", type=int, default=1)
@@ -752,10 +764,21 @@ def main() -> int:
         stop.record(stream)
         stop.synchronize()
         torch.cuda.synchronize()
+        if graph is not None:
+            # the spread: the same graph replayed REPEATS more times, each timed alone
+            for _ in range(REPEATS):
+                a = torch.cuda.Event(enable_timing=True)
+                z = torch.cuda.Event(enable_timing=True)
+                a.record(stream)
+                graph.replay()
+                z.record(stream)
+                z.synchronize()
+                repeat_s.append(a.elapsed_time(z) / 1e3)
         return start.elapsed_time(stop) / 1e3
 
     # stream launches, then (by default) the same steps replayed from one graph,
     # the way a serving engine runs its decode steps; `value` is the graph replay
+    repeat_s: list[float] = []
     modes = {"both": (True, True), "stream": (True, False), "graph": (False, True)}[args.launch]
     stream_s = time_steps(False) if modes[0] else None
     graph_s = time_steps(True) if modes[1] else None
@@ -821,7 +844,16 @@ def main() -> int:
             "avg_launch_us": round(call_s * 1e6, 3),
         },
         "setup_s": round(setup_s, 1),
+        "device": device_info(torch, dev),
     }
+    if repeat_s:
+        rates = sorted(total_bytes / t / 1e9 for t in repeat_s)
+        result["graph_repeats"] = {
+            "n": len(rates),
+            "median_gbs": round(float(np.median(rates)), 2),
+            "min_gbs": round(rates[0], 2),
+            "max_gbs": round(rates[-1], 2),
+        }
     if graph_s is not None and stream_s is not None:
         result["stream_launches"] = {
             "value": round(total_bytes / stream_s / 1e9, 2),

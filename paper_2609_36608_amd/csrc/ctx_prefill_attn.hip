@@ -77,6 +77,14 @@ __device__ __forceinline__ void split_bf16x2(float a, float b, uint32_t* hi, uin
   *lo = pack_bf16x2(a - __uint_as_float(ua & 0xffff0000u), b - __uint_as_float(ub & 0xffff0000u));
 }
 
+// Largest of 8 logits with the NaN-propagating maximum, which gfx950 has as a
+// three-input instruction (fmaxf would first quiet each input).  A NaN logit
+// gives a NaN weight either way.
+__device__ __forceinline__ float max8(float a, float b, float c, float d, float e, float f, float g, float h) {
+  const auto mx = [](float x, float y) { return __builtin_elementwise_maximum(x, y); };
+  return mx(mx(mx(a, b), mx(c, d)), mx(mx(e, f), mx(g, h)));
+}
+
 template <typename OutT, bool kSplitP>
 __global__ __launch_bounds__(64 * kPrefillWaves) __attribute__((amdgpu_waves_per_eu(2))) void prefill_kernel(
     const uint16_t* __restrict__ q, const uint16_t* __restrict__ kc, const uint16_t* __restrict__ vc,
@@ -238,10 +246,10 @@ __global__ __launch_bounds__(64 * kPrefillWaves) __attribute__((amdgpu_waves_per
 #pragma unroll
             for (int i = 0; i < 4; ++i)
               x[4 * h + i] = (t0 + 16 * h + 4 * c + i > last_pos[ct]) ? -INFINITY : sc[ct][h][i] * cs;
-          lmax = fmaxf(fmaxf(fmaxf(x[0], x[1]), fmaxf(x[2], x[3])), fmaxf(fmaxf(x[4], x[5]), fmaxf(x[6], x[7])));
+          lmax = max8(x[0], x[1], x[2], x[3], x[4], x[5], x[6], x[7]);
         } else {
           const f32x4 a = sc[ct][0], e = sc[ct][1];
-          lmax = fmaxf(fmaxf(fmaxf(a[0], a[1]), fmaxf(a[2], a[3])), fmaxf(fmaxf(e[0], e[1]), fmaxf(e[2], e[3]))) * cs;
+          lmax = max8(a[0], a[1], a[2], a[3], e[0], e[1], e[2], e[3]) * cs;
         }
         // lazy rescale: only when some logit exceeds the running max by 2^8;
         // the column max (across the 4 lanes of a column) only then
@@ -275,14 +283,17 @@ __global__ __launch_bounds__(64 * kPrefillWaves) __attribute__((amdgpu_waves_per
             plo[ct][j] = lw;
           }
         } else {
-          // one bf16 term; the row sum adds the rounded weights the product uses
-          float rs[4];
+          // one bf16 term; the row sum adds the rounded weights the product
+          // uses, a pair per dot product with (1, 1)
+          const bf16x2 ones = {(__bf16)1.0f, (__bf16)1.0f};
+          float l = st[ct].l;
 #pragma unroll
           for (int j = 0; j < 4; ++j) {
-            phi[ct][j] = pack_bf16x2(pr[2 * j], pr[2 * j + 1]);
-            rs[j] = __uint_as_float(phi[ct][j] << 16) + __uint_as_float(phi[ct][j] & 0xffff0000u);
+            const bf16x2 pair = {(__bf16)pr[2 * j], (__bf16)pr[2 * j + 1]};  // round to nearest even
+            phi[ct][j] = __builtin_bit_cast(uint32_t, pair);
+            l = __builtin_amdgcn_fdot2_f32_bf16(pair, ones, l, false);
           }
-          st[ct].l += (rs[0] + rs[1]) + (rs[2] + rs[3]);
+          st[ct].l = l;
         }
       }
       // O^T += V^T P^T: the K dimension holds tokens 4c..4c+3 of both halves.
