@@ -161,8 +161,14 @@ __global__ __launch_bounds__(64 * kPrefillWaves) __attribute__((amdgpu_waves_per
 
   Softmax st[kPrefillTiles];
   f32x4 o[kPrefillTiles][8];
+  // lazy-rescale thresholds: the running max plus 2^8, in log2 units (for
+  // masked blocks, whose logits are scaled first) and divided by cs (for the
+  // raw logits of unmasked blocks); both move only with the running max
+  float thr[kPrefillTiles], thr_raw[kPrefillTiles];
 #pragma unroll
   for (int ct = 0; ct < kPrefillTiles; ++ct) {
+    thr[ct] = -INFINITY;
+    thr_raw[ct] = -INFINITY;
     st[ct] = Softmax{-INFINITY, 0.f};
 #pragma unroll
     for (int nb = 0; nb < 8; ++nb) o[ct][nb] = f32x4{0.f, 0.f, 0.f, 0.f};
@@ -240,6 +246,7 @@ __global__ __launch_bounds__(64 * kPrefillWaves) __attribute__((amdgpu_waves_per
       for (int ct = 0; ct < kPrefillTiles; ++ct) {
         float x[8];
         float lmax;
+        bool grow;
         if (masked) {  // blocks on the causal diagonal (or past kv_end)
 #pragma unroll
           for (int h = 0; h < 2; ++h)
@@ -247,13 +254,16 @@ __global__ __launch_bounds__(64 * kPrefillWaves) __attribute__((amdgpu_waves_per
             for (int i = 0; i < 4; ++i)
               x[4 * h + i] = (t0 + 16 * h + 4 * c + i > last_pos[ct]) ? -INFINITY : sc[ct][h][i] * cs;
           lmax = max8(x[0], x[1], x[2], x[3], x[4], x[5], x[6], x[7]);
+          grow = lmax > thr[ct];
         } else {
           const f32x4 a = sc[ct][0], e = sc[ct][1];
-          lmax = max8(a[0], a[1], a[2], a[3], e[0], e[1], e[2], e[3]) * cs;
+          lmax = max8(a[0], a[1], a[2], a[3], e[0], e[1], e[2], e[3]);
+          grow = lmax > thr_raw[ct];
         }
         // lazy rescale: only when some logit exceeds the running max by 2^8;
         // the column max (across the 4 lanes of a column) only then
-        if (__any(lmax > st[ct].m + kLazyRescale)) {
+        if (__any(grow)) {
+          if (!masked) lmax *= cs;
           float mx = fmaxf(lmax, __shfl_xor(lmax, 16));
           mx = fmaxf(mx, __shfl_xor(mx, 32));
           const float m_new = fmaxf(st[ct].m, mx);
@@ -262,6 +272,8 @@ __global__ __launch_bounds__(64 * kPrefillWaves) __attribute__((amdgpu_waves_per
 #pragma unroll
           for (int nb = 0; nb < 8; ++nb) o[ct][nb] *= alpha;
           st[ct].m = m_new;
+          thr[ct] = m_new + kLazyRescale;
+          thr_raw[ct] = thr[ct] / cs;  // +inf for a zero scale: all logits are 0 then
         }
         float pr[8];
         if (masked) {
