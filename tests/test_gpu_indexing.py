@@ -86,10 +86,13 @@ def test_spike_retrieval_exact_rows():
 
 
 def test_gqa_mapping_exact():
-    """V = kv index on each KV head -> out[b, h, :] = h // g for every group size."""
+    """V = kv index on each KV head -> out[b, h, :] = h // g for every group size.
+    Odd head counts leave the last pair of heads of the merge with one head,
+    and odd group sizes put a pair's two heads on different KV heads."""
     rng = np.random.default_rng(23)
-    # Hkv 8, 4 -> four KV heads per workgroup; 2, 6 -> two; 1, 3 -> one
-    for hq, hkv in [(32, 8), (16, 8), (8, 8), (16, 1), (32, 2), (64, 4), (12, 6), (12, 3)]:
+    # Hkv 8, 4 -> four KV heads per workgroup; 2, 6 -> two; 1, 3, 7, 5 -> one
+    for hq, hkv in [(32, 8), (16, 8), (8, 8), (16, 1), (32, 2), (64, 4), (12, 6), (12, 3), (9, 3), (7, 7),
+                    (5, 1)]:
         lens = np.array([3, 40, 129], np.int32)
         lay = wl.make_layout(lens, 1)
         k = rand_bits(rng, (lay.num_rows, hkv, 128))
@@ -97,10 +100,33 @@ def test_gqa_mapping_exact():
         for kv in range(hkv):
             v[:, kv] = bf(np.array([float(kv)], np.float32))[0]
         q = rand_bits(rng, (3, hq, 128))
-        got = run(hq, hkv, q, k, v, lay.offsets, lens, 0.0884)
         g = hq // hkv
-        for h in range(hq):
-            np.testing.assert_allclose(got[:, h], float(h // g), rtol=1e-5, atol=1e-6, err_msg=f"{hq}/{hkv} h={h}")
+        for split in (0, 16):
+            got = run(hq, hkv, q, k, v, lay.offsets, lens, 0.0884, split_tokens=split)
+            for h in range(hq):
+                np.testing.assert_allclose(got[:, h], float(h // g), rtol=1e-5, atol=1e-6,
+                                           err_msg=f"{hq}/{hkv} h={h} split={split}")
+
+
+def test_more_than_256_sequences():
+    """300 sequences: the kernels scan the lengths 256 at a time, so the range
+    search and the merge cross a chunk boundary; empty sequences sit at both
+    ends of each chunk and a long one straddles the boundary."""
+    rng = np.random.default_rng(29)
+    hq, hkv = 32, 8
+    lens = rng.integers(1, 400, size=300).astype(np.int32)
+    lens[[0, 255, 256, 299]] = 0
+    lens[[1, 254, 257]] = [1, 2500, 3]
+    lay = wl.make_layout(lens, 1, gap_max=7, shuffle=True, rng=rng)
+    k = rand_bits(rng, (lay.num_rows, hkv, 128))
+    v = rand_bits(rng, (lay.num_rows, hkv, 128))
+    q = rand_bits(rng, (len(lens), hq, 128))
+    ref = oracle.decode_attn(q, k, v, lay.offsets, lens, 0.0884)
+    for split in (0, 48):
+        got = run(hq, hkv, q, k, v, lay.offsets, lens, 0.0884, split_tokens=split, max_seq_len=lay.max_seq_len,
+                  canary=True)
+        assert_parity(got, ref, f"300 sequences split={split}")
+        assert (got[lens == 0] == 0).all(), "empty sequences must give zeros"
 
 
 @pytest.mark.parametrize("C", [16, 64, 256])

@@ -180,6 +180,20 @@ def test_paged_abi_errors():
             DecodeAttention(16, 8, 2, 32, **kw)
 
 
+def test_paged_more_than_256_sequences_with_append():
+    """300 sequences in 16-token pages: the padded range plan and the merge scan
+    the lengths across a 256-sequence chunk boundary; the append of every
+    sequence's newest token is checked in the caches too."""
+    w, lay, q, kp, vp, bt, rng = paged_case(37, 16, batch=300, hi=300)
+    k_new = rand_bits(rng, (w.batch, w.num_kv_heads, 128))
+    v_new = rand_bits(rng, (w.batch, w.num_kv_heads, 128))
+    ref = oracle.decode_attn_paged(q, kp, vp, bt, lay.lens, w.scale, k_new, v_new)
+    for split in (0, 32):
+        got, _, _ = run_paged(w, q, kp, vp, bt, lay.lens, 16, split=split, k_new=k_new, v_new=v_new,
+                              max_seq_len=lay.max_seq_len)
+        assert_parity(got, ref, f"paged append, 300 sequences, split={split}")
+
+
 def test_paged_bf16_output_and_many_sequences():
     """bf16 output equals the rounded fp32 output, and a batch of more than
     64 sequences (the range search over the whole batch) with an append."""
