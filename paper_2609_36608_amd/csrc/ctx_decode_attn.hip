@@ -96,8 +96,11 @@ __device__ __forceinline__ float wave_max(float x) {
   return x;
 }
 
-// Tokens a sequence of length len occupies in the flattened batch.
-__device__ __forceinline__ int64_t padded(int64_t len, int pad) { return (len + pad - 1) / pad * pad; }
+// Tokens a sequence of length len occupies in the flattened batch.  pad is 1
+// (contiguous caches) or kBlock (paged), a power of two, so rounding up is a
+// mask: a 64-bit division by a run-time value is a long instruction sequence
+// on the critical path of every wave's length scan.
+__device__ __forceinline__ int64_t padded(int64_t len, int pad) { return (len + pad - 1) & ~(int64_t)(pad - 1); }
 
 // sum of the padded lens[0 .. n)
 __device__ __forceinline__ int64_t sum_lens(const int32_t* __restrict__ lens, int n, int lane, int pad) {
