@@ -68,9 +68,11 @@ def profiled_traffic(workload: str, kernel: str = "decode_split_kernel"):
     return None
 
 
-def cpu_baseline(w: wl.Workload, layout: wl.Layout, target_s: float, threads: int) -> dict:
+def cpu_baseline(w: wl.Workload, layout: wl.Layout, target_s: float, threads: int,
+                 single_thread_s: float = 3.0) -> dict:
     """Time the CPU oracle on layer 0 / step 0 for a fixed sample of sequences,
-    repeated until about target_s seconds of CPU work have run."""
+    repeated until about target_s seconds of CPU work have run on `threads`
+    threads, then for about single_thread_s seconds on one thread."""
     import oracle
 
     rng = np.random.default_rng(7)
@@ -97,6 +99,14 @@ def cpu_baseline(w: wl.Workload, layout: wl.Layout, target_s: float, threads: in
         if el >= target_s or el / reps * (reps + 1) > 3 * target_s:
             break
     gbs = nbytes * reps / el / 1e9
+    # the same sample on one thread, for a shorter while
+    reps1, t1 = 0, time.perf_counter()
+    while True:
+        oracle.decode_attn(q, k, v, offs, sl, w.scale, threads=1)
+        reps1 += 1
+        el1 = time.perf_counter() - t1
+        if el1 >= single_thread_s:
+            break
     full_step_bytes = algorithmic_bytes(lens, w) * w.layers
     return {
         "value": round(gbs, 4),
@@ -107,7 +117,21 @@ def cpu_baseline(w: wl.Workload, layout: wl.Layout, target_s: float, threads: in
                    f"({int(sl.sum())} tokens), all {w.num_q_heads} heads, run {reps}x in {el:.1f} s; "
                    f"float64 C oracle, OpenMP over (sequence, head)"),
         "decode_steps_per_s": round(gbs * 1e9 / full_step_bytes, 6),
+        "single_thread": {"value": round(nbytes * reps1 / el1 / 1e9, 4), "unit": "GB/s", "cores": 1,
+                          "runs": reps1, "seconds": round(el1, 1)},
+        "cpu_model": cpu_model(),
     }
+
+
+def cpu_model() -> str:
+    """The host CPU's model name as /proc/cpuinfo reports it ("" if unreadable)."""
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return ""
 
 
 PREFILL_METRIC = "causal prefill attention TFLOP/s (fraction of 2.5 PFLOP/s bf16 MFMA peak), 1 MI355X"

@@ -37,3 +37,14 @@ def test_more_than_one_gpu_is_refused():
     assert r.returncode == 2
     assert "one GPU" in r.stderr
     assert r.stdout == ""
+
+
+def test_cpu_baseline_reports_threads_single_thread_and_model():
+    # the oracle baseline on the tiny batch: the multi-thread and one-thread rates
+    # over the same sample, the thread counts used, and the host CPU's model
+    w = wl.WORKLOADS["tiny"]
+    r = bench.cpu_baseline(w, wl.workload_layout(w), 0.2, 2, single_thread_s=0.1)
+    assert r["kind"] == "oracle" and r["cores"] == 2 and r["unit"] == "GB/s" and r["value"] > 0
+    assert r["single_thread"]["cores"] == 1 and r["single_thread"]["value"] > 0
+    assert r["single_thread"]["runs"] >= 1
+    assert isinstance(r["cpu_model"], str)
