@@ -172,10 +172,9 @@ int ctx_decode_attn_run_paged(ctx_decode_attn* handle, const void* q, void* k_pa
  *                weights as two bf16 terms (16 significant bits; about 1e-6
  *                absolute) at half again the matrix-core work.
  *   out          [total_q, Hq, D] of desc.out_dtype; rows of no sequence are untouched
- * Needs a group size Hq / Hkv dividing 16 (UNSUPPORTED otherwise).  No
- * workspace, no allocation, no host sync; deterministic.
- * Errors: INVALID_ARG (also for unknown flag bits), UNSUPPORTED, CAPACITY,
- * ALIGNMENT, HIP.
+ * Any group size the handle accepts (Hq / Hkv <= 16).  No workspace, no
+ * allocation, no host sync; deterministic.
+ * Errors: INVALID_ARG (also for unknown flag bits), CAPACITY, ALIGNMENT, HIP.
  */
 #define CTX_PREFILL_SPLIT_P 1u
 int ctx_prefill_attn_run(ctx_decode_attn* handle, const void* q, const void* k_cache, const void* v_cache,

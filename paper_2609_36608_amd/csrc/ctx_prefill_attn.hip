@@ -3,9 +3,10 @@
 //
 // Causal prefill of each sequence's newest tokens (the reference next
 // observation the fast action conditions on) against its cache, which already
-// holds their K/V rows.  Query column n of a 16-column MFMA tile is query
-// position n / g, head n % g of one KV group (g divides 16), so every column
-// carries work.  A workgroup of kPrefillWaves waves covers kPrefillCols
+// holds their K/V rows.  The columns of the 16-column MFMA tiles are the
+// consecutive (query position, head) pairs of one KV group, column c being
+// position c / g and head c % g, so every column carries work for any group
+// size g (a position's heads may straddle two workgroups).  A workgroup of kPrefillWaves waves covers kPrefillCols
 // columns of one (sequence, KV head) and streams 32-token K/V blocks, up to
 // its last query position, through a three-stage LDS tile that all its
 // waves share; the blocks are loaded straight into LDS, two blocks ahead of
@@ -106,11 +107,13 @@ __global__ __launch_bounds__(64 * kPrefillWaves) __attribute__((amdgpu_waves_per
   const int kv = unit % pp.hkv;
   const int b = unit / pp.hkv;
   const int nq = q_lens[b];
-  const int first_q = tile * (kPrefillCols / g);
+  // query positions of the workgroup's columns tile * kPrefillCols ..
+  const int first_q = tile * kPrefillCols / g;
   if (first_q >= nq) return;  // the whole workgroup: nothing to do
   const int seq_len = lens[b];
   const int hist = seq_len - nq;  // position of query 0
-  const int last_q = (first_q + kPrefillCols / g < nq ? first_q + kPrefillCols / g : nq) - 1;
+  const int col_last_q = (tile * kPrefillCols + kPrefillCols - 1) / g;
+  const int last_q = col_last_q < nq - 1 ? col_last_q : nq - 1;
   const int kv_end = hist + last_q + 1;  // tokens any query of the workgroup attends to
   const size_t row_elems = (size_t)pp.hkv * kHeadDim;
   const int row_bytes = (int)(row_elems * 2);
@@ -364,8 +367,6 @@ extern "C" int ctx_prefill_attn_run(ctx_decode_attn* h, const void* q, const voi
   if (rc != CTX_OK) return rc;
   const ctx_decode_attn_desc& d = h->desc;
   const int g = d.num_q_heads / d.num_kv_heads;
-  if (16 % g != 0)
-    return fail(CTX_ERR_UNSUPPORTED, "prefill needs a group size dividing 16 (got %d)", g);
   if (max_q_len < 0) return fail(CTX_ERR_INVALID_ARG, "max_q_len %d < 0", max_q_len);
   if ((flags & ~CTX_PREFILL_SPLIT_P) != 0) return fail(CTX_ERR_INVALID_ARG, "unknown prefill flags 0x%x", flags);
   if (num_seqs == 0 || max_q_len == 0) return CTX_OK;

@@ -61,7 +61,8 @@ MODES = [pytest.param(False, id="bf16p"), pytest.param(True, id="splitp")]
 
 
 @pytest.mark.parametrize("split_p", MODES)
-@pytest.mark.parametrize("hq,hkv", [(32, 8), (16, 8), (16, 16), (16, 1), (64, 8)])
+@pytest.mark.parametrize("hq,hkv", [(32, 8), (16, 8), (16, 16), (16, 1), (64, 8), (24, 8), (28, 4), (40, 8),
+                                    (12, 2), (14, 2)])
 def test_prefill_parity(hq, hkv, split_p):
     w, lay, lens, nq, qs, q, k, v = prefill_case(hq * 3 + hkv, hq, hkv, batch=7, hist=(0, 500), new=(1, 140))
     nq[0], nq[1] = 1, 128 // (hq // hkv) + 1  # decode-like and one past a workgroup tile
@@ -173,15 +174,6 @@ def test_prefill_full_size_act_first_burst_sampled():
 
 def test_prefill_abi():
     lib = bd.load_library()
-    with DecodeAttention(24, 8, 2, 32) as attn:  # group 3 does not divide 16
-        z = torch.zeros((2, 24, 128), dtype=torch.bfloat16, device=dev())
-        kv = torch.zeros((8, 8, 128), dtype=torch.bfloat16, device=dev())
-        i = torch.zeros(2, dtype=torch.int32, device=dev())
-        o = torch.zeros((2, 24, 128), dtype=torch.float32, device=dev())
-        with pytest.raises(CtxError):
-            attn.prefill(z, kv, kv, i, i, i, i, 1, 0.1, o)
-        with pytest.raises(CtxError):
-            attn.prefill(z, kv, kv, i, i, i, i, 1, 0.1, o, split_p=True)
     with DecodeAttention(32, 8, 2, 32) as attn:
         h = attn.handle
         z = torch.zeros((2, 32, 128), dtype=torch.bfloat16, device=dev())
