@@ -107,13 +107,15 @@ __global__ __launch_bounds__(64 * kPrefillWaves) __attribute__((amdgpu_waves_per
   const int kv = unit % pp.hkv;
   const int b = unit / pp.hkv;
   const int nq = q_lens[b];
-  // query positions of the workgroup's columns tile * kPrefillCols ..
+  // query positions of the workgroup's columns, tile * kPrefillCols onwards
   const int first_q = tile * kPrefillCols / g;
   if (first_q >= nq) return;  // the whole workgroup: nothing to do
   const int seq_len = lens[b];
   const int hist = seq_len - nq;  // position of query 0
-  const int col_last_q = (tile * kPrefillCols + kPrefillCols - 1) / g;
-  const int last_q = col_last_q < nq - 1 ? col_last_q : nq - 1;
+  // one past the last column's position; min(q_end, nq) - 1 rather than
+  // min(q_end - 1, nq - 1), a form that compiles to 8 more registers
+  const int q_end = (tile * kPrefillCols + kPrefillCols - 1) / g + 1;
+  const int last_q = (q_end < nq ? q_end : nq) - 1;
   const int kv_end = hist + last_q + 1;  // tokens any query of the workgroup attends to
   const size_t row_elems = (size_t)pp.hkv * kHeadDim;
   const int row_bytes = (int)(row_elems * 2);
