@@ -62,7 +62,7 @@ MODES = [pytest.param(False, id="bf16p"), pytest.param(True, id="splitp")]
 
 @pytest.mark.parametrize("split_p", MODES)
 @pytest.mark.parametrize("hq,hkv", [(32, 8), (16, 8), (16, 16), (16, 1), (64, 8), (24, 8), (28, 4), (40, 8),
-                                    (12, 2), (14, 2)])
+                                    (12, 2), (14, 2), (18, 2), (20, 2), (24, 2), (30, 2)])
 def test_prefill_parity(hq, hkv, split_p):
     w, lay, lens, nq, qs, q, k, v = prefill_case(hq * 3 + hkv, hq, hkv, batch=7, hist=(0, 500), new=(1, 140))
     nq[0], nq[1] = 1, 128 // (hq // hkv) + 1  # decode-like and one past a workgroup tile
