@@ -68,6 +68,13 @@ def profiled_traffic(workload: str, kernel: str = "decode_split_kernel"):
     return None
 
 
+def traffic_fields(workload: str, kernel: str = "decode_split_kernel") -> dict:
+    """The roofline's `traffic` (HBM bytes per launch from the counters, or
+    None) and, beside it, where that figure comes from."""
+    d = profiled_traffic(workload, kernel)
+    return {"traffic": d["bytes_per_launch"] if d else None, "traffic_detail": d}
+
+
 def cpu_baseline(w: wl.Workload, layout: wl.Layout, target_s: float, threads: int,
                  single_thread_s: float = 3.0) -> dict:
     """Time the CPU oracle on layer 0 / step 0 for a fixed sample of sequences,
@@ -296,7 +303,7 @@ def bench_prefill(args) -> int:
             "peak": MFMA_BF16_PEAK_TFLOPS,
             "unit": "TFLOP/s",
             "frac": round(flops / (elapsed_s / calls) / 1e12 / MFMA_BF16_PEAK_TFLOPS, 4),
-            "traffic": profiled_traffic(w.name, "prefill_kernel"),
+            **traffic_fields(w.name, "prefill_kernel"),
             "kernel": ("prefill_kernel (one ctx_prefill_attn_run call per layer, "
                        + ("two-term softmax weights)" if args.prefill_p == "split" else "bf16 softmax weights)")),
             "flops_per_launch": flops,
@@ -445,7 +452,7 @@ def bench_opd(args) -> int:
             "peak": HBM_PEAK_GBS,
             "unit": "GB/s",
             "frac": round(gbs / HBM_PEAK_GBS, 4),
-            "traffic": profiled_traffic(w.name, "opd_row_kernel"),
+            **traffic_fields(w.name, "opd_row_kernel"),
             "kernel": "opd_row_kernel (+ opd_weight_kernel, opd_reduce_kernel: one ctx_opd_loss_run call)",
             "bytes_per_launch": nbytes,
             "avg_launch_us": round(call_s * 1e6, 3),
@@ -862,7 +869,7 @@ def main() -> int:
             "peak": HBM_PEAK_GBS,
             "unit": "GB/s",
             "frac": round(per_call_bytes / call_s / 1e9 / HBM_PEAK_GBS, 4),
-            "traffic": profiled_traffic(w.name),
+            **traffic_fields(w.name),
             "kernel": "one ctx_decode_attn_run call (decode_split_kernel + decode_merge_kernel)",
             "bytes_per_launch": round(per_call_bytes),
             "avg_launch_us": round(call_s * 1e6, 3),

@@ -48,3 +48,26 @@ def test_cpu_baseline_reports_threads_single_thread_and_model():
     assert r["single_thread"]["cores"] == 1 and r["single_thread"]["value"] > 0
     assert r["single_thread"]["runs"] >= 1
     assert isinstance(r["cpu_model"], str)
+
+
+def test_roofline_traffic_is_bytes_per_launch_from_a_current_profile():
+    """`traffic` is a plain byte count, taken from a committed counter summary
+    only while the kernel source still hashes to the one it records."""
+    import glob
+    import hashlib
+
+    paths = glob.glob(os.path.join(ROOT, "profiles", "*hbm_traffic*.md"))
+    assert paths
+    for path in paths:
+        fields = dict(line.strip().split(": ", 1) for line in open(path)
+                      if line.startswith(("kernel", "workload", "traffic_bytes")) and ": " in line)
+        src = fields.get("kernel_source", "paper_2609_36608_amd/csrc/ctx_decode_attn.hip")
+        current = hashlib.sha256(open(os.path.join(ROOT, src), "rb").read()).hexdigest()
+        got = bench.traffic_fields(fields["workload"], fields.get("kernel", "decode_split_kernel"))
+        if current == fields["kernel_source_sha256"]:
+            assert got["traffic"] == int(fields["traffic_bytes_per_launch"])
+            assert isinstance(got["traffic"], int)
+            assert got["traffic_detail"]["source"] == os.path.relpath(path, ROOT)
+        else:
+            assert got == {"traffic": None, "traffic_detail": None}
+    assert bench.traffic_fields("no_such_workload") == {"traffic": None, "traffic_detail": None}
