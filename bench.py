@@ -869,7 +869,7 @@ def main() -> int:
             "peak": HBM_PEAK_GBS,
             "unit": "GB/s",
             "frac": round(per_call_bytes / call_s / 1e9 / HBM_PEAK_GBS, 4),
-            **traffic_fields(w.name),
+            **traffic_fields(w.name, f"decode_split_kernel paged {args.paged}" if args.paged else "decode_split_kernel"),
             "kernel": "one ctx_decode_attn_run call (decode_split_kernel + decode_merge_kernel)",
             "bytes_per_launch": round(per_call_bytes),
             "avg_launch_us": round(call_s * 1e6, 3),
