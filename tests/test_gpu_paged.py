@@ -95,11 +95,26 @@ def test_paged_append(page_tokens, split):
 
 
 def test_paged_gqa_group_sizes():
-    for hq, hkv in [(16, 1), (64, 4), (8, 8)]:
-        w, lay, q, kp, vp, bt, _ = paged_case(90 + hq, 16, batch=5, hq=hq, hkv=hkv, hi=300)
+    """Workgroups of up to 8 KV heads: odd KV-head counts leave a partial
+    workgroup, and odd group sizes an odd number of query heads per KV head;
+    every case also appends, so the append's row addressing is checked too."""
+    for hq, hkv in [(16, 1), (64, 4), (8, 8), (9, 3), (12, 6), (5, 1), (28, 7), (45, 9), (30, 10)]:
+        w, lay, q, kp, vp, bt, rng = paged_case(90 + hq + hkv, 16, batch=5, hq=hq, hkv=hkv, hi=300)
         ref = oracle.decode_attn_paged(q, kp, vp, bt, lay.lens, w.scale)
         got, _, _ = run_paged(w, q, kp, vp, bt, lay.lens, 16)
         assert_parity(got, ref, f"paged {hq}/{hkv}")
+        k_new = rand_bits(rng, (w.batch, hkv, 128))
+        v_new = rand_bits(rng, (w.batch, hkv, 128))
+        kp_exp, vp_exp = kp.copy(), vp.copy()
+        for b in range(w.batch):
+            t = lay.lens[b] - 1
+            kp_exp[bt[b, t // 16], t % 16] = k_new[b]
+            vp_exp[bt[b, t // 16], t % 16] = v_new[b]
+        ref = oracle.decode_attn_paged(q, kp, vp, bt, lay.lens, w.scale, k_new, v_new)
+        got, kp2, vp2 = run_paged(w, q, kp, vp, bt, lay.lens, 16, split=32, k_new=k_new, v_new=v_new)
+        assert_parity(got, ref, f"paged append {hq}/{hkv}")
+        np.testing.assert_array_equal(kp2, kp_exp)
+        np.testing.assert_array_equal(vp2, vp_exp)
 
 
 def test_paged_full_size_long_ragged_with_append():
