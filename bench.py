@@ -219,8 +219,7 @@ def bench_prefill(args) -> int:
     for i in range(n_buf):
         k = torch.empty((layout.num_rows, w.num_kv_heads, w.head_dim), dtype=torch.bfloat16, device=dev)
         v = torch.empty_like(k)
-        wl.fill_normal_bf16_device(k, wl.DEFAULT_SEED, w.index, i, 1)
-        wl.fill_normal_bf16_device(v, wl.DEFAULT_SEED, w.index, i, 2)
+        wl.fill_kv_device(k, v, w, i)
         ks.append(k)
         vs.append(v)
     total_q = int(nq.sum())
@@ -711,8 +710,7 @@ def main() -> int:
     for i in range(n_buf):
         k = torch.empty((cache_rows, w.num_kv_heads, w.head_dim), dtype=torch.bfloat16, device=dev)
         v = torch.empty_like(k)
-        wl.fill_normal_bf16_device(k, wl.DEFAULT_SEED, w.index, i, 1)
-        wl.fill_normal_bf16_device(v, wl.DEFAULT_SEED, w.index, i, 2)
+        wl.fill_kv_device(k, v, w, i)  # N(0,1), plus the workload's peaky keys
         ks.append(k)
         vs.append(v)
     qs = []

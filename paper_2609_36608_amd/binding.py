@@ -330,6 +330,8 @@ def opd_loss(logits, tokens, old_logp, teacher_logp, mask, seq_starts, params: O
             raise ValueError(f"{name} must be a contiguous vector")
     out = dict(out or {})
     vocab = int(out.pop("vocab", logits.shape[1]))
+    if not 0 < vocab <= logits.shape[1]:
+        raise ValueError(f"vocab {vocab} must be in 1..{logits.shape[1]} (the columns of logits)")
 
     def buf(name, shape, dtype):
         t = out.get(name)
@@ -347,8 +349,9 @@ def opd_loss(logits, tokens, old_logp, teacher_logp, mask, seq_starts, params: O
         g = out.get("grad_logits")
         if g is None:  # rows padded to a multiple of 8 elements (16-byte chunks)
             g = torch.empty((n, (vocab + 7) // 8 * 8), dtype=torch.bfloat16, device=dev)
-        elif g.dtype != torch.bfloat16 or g.dim() != 2 or g.shape[0] != n or g.stride(1) != 1:
-            raise ValueError("out['grad_logits'] must be bf16 [N, >= vocab] with unit column stride")
+        elif (g.dtype != torch.bfloat16 or g.dim() != 2 or g.shape[0] != n or g.stride(1) != 1
+              or g.shape[1] < vocab or g.device != dev):
+            raise ValueError(f"out['grad_logits'] must be bf16 [N, >= {vocab}] with unit column stride on {dev}")
         res["grad_logits"] = g if out.get("grad_logits") is not None else g[:, :vocab]
     sp = _stream_ptr(stream, dev)
     rc = lib.ctx_opd_loss_run(logits.data_ptr(), logits.stride(0), vocab, tokens.data_ptr(), old_logp.data_ptr(),

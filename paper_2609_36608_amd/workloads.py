@@ -270,21 +270,51 @@ def small_workload(base: Workload, *, name: str | None = None, batch: int | None
 
 # ------------------------------------------------------ device-side filling
 
-def fill_normal_bf16_device(t, seed: int, *key: int) -> None:
-    """Fill a CUDA bf16 tensor with N(0,1) values from torch's seeded device
-    generator (used for rows that no oracle check reads)."""
+def _device_generator(device, seed: int, *key: int):
     import torch
 
-    g = torch.Generator(device=t.device)
+    g = torch.Generator(device=device)
     h = 0
     for x in (seed, *key):
         h = (h * 1000003 + int(x) + 1) % (2**63 - 1)
     g.manual_seed(h)
+    return g
+
+
+def fill_normal_bf16_device(t, seed: int, *key: int) -> None:
+    """Fill a CUDA bf16 tensor with N(0,1) values from torch's seeded device
+    generator (full-size layers; tests copy them to the host for the oracle)."""
+    g = _device_generator(t.device, seed, *key)
     flat = t.view(-1)
     chunk = 1 << 28
     for s in range(0, flat.numel(), chunk):
         e = min(s + chunk, flat.numel())
         flat[s:e].normal_(generator=g)
+
+
+def apply_peaky_keys_device(k, w: Workload, layer: int, seed: int = DEFAULT_SEED) -> None:
+    """Multiply each cache row's key (all heads and dims) by `peaky_gain` with
+    probability `peaky_frac`, drawn on the device; no-op for workloads without
+    peaky keys.  k is [rows, Hkv, D] or paged [pages, P, Hkv, D] bf16; a
+    power-of-two gain is exact in bf16."""
+    import torch
+
+    if w.peaky_frac <= 0:
+        return
+    rows = k.numel() // (w.num_kv_heads * w.head_dim)
+    g = _device_generator(k.device, seed, w.index, layer, _T_MASK)
+    peaky = torch.rand(rows, generator=g, device=k.device) < w.peaky_frac
+    gain = torch.ones(rows, dtype=torch.bfloat16, device=k.device)
+    gain.masked_fill_(peaky, w.peaky_gain)
+    k.view(rows, -1).mul_(gain[:, None])
+
+
+def fill_kv_device(k, v, w: Workload, layer: int, seed: int = DEFAULT_SEED) -> None:
+    """A full-size layer's caches drawn on the device: N(0,1) bf16 keys and
+    values, and the workload's peaky keys."""
+    fill_normal_bf16_device(k, seed, w.index, layer, 1)
+    fill_normal_bf16_device(v, seed, w.index, layer, 2)
+    apply_peaky_keys_device(k, w, layer, seed)
 
 
 # ----------------------------------------------------------------- OPD loss batches

@@ -53,7 +53,8 @@ class SampledLayer:
         lay = self.layout
         rng = np.random.default_rng(1000 + w.index)
         lens = lay.lens
-        picks = {int(np.argmax(lens)), int(np.argmin(lens))}
+        # the longest, the shortest and the one placed last (highest cache offsets)
+        picks = {int(np.argmax(lens)), int(np.argmin(lens)), int(np.argmax(lay.offsets))}
         others = [b for b in range(w.batch) if b not in picks]
         picks |= set(int(x) for x in rng.choice(others, size=min(n_sample - len(picks), len(others)), replace=False))
         self.sample = sorted(picks)

@@ -129,49 +129,6 @@ def test_prefill_last_row_equals_decode():
     assert_parity(got[last], dec, "bf16 weights against the decode kernel", tight=False)
 
 
-def test_prefill_full_size_act_first_burst_sampled():
-    """Act-first burst shape: 256 sequences, history U{4096..12288} plus an
-    appended reference observation of U{128..512} tokens, prefilled in one
-    call.  Sampled query rows are recomputed by the oracle as decodes of
-    their prefixes."""
-    w = wl.WORKLOADS["act_first_burst"]
-    rng = np.random.default_rng(17)
-    lens = wl.draw_lengths(w)                       # history + reference observation
-    nq = wl.draw_extra(w)
-    lay = wl.make_layout(lens, 1)
-    k = torch.empty((lay.num_rows, 8, 128), dtype=torch.bfloat16, device=dev())
-    v = torch.empty_like(k)
-    wl.fill_normal_bf16_device(k, 42, w.index, 0, 11)
-    wl.fill_normal_bf16_device(v, 42, w.index, 0, 12)
-    q_starts = np.concatenate([[0], np.cumsum(nq)[:-1]]).astype(np.int32)
-    total_q = int(nq.sum())
-    q = rand_bits(rng, (total_q, 32, 128))
-    out = torch.empty((total_q, 32, 128), dtype=torch.float32, device=dev())
-    out_split = torch.empty_like(out)
-    with DecodeAttention(32, 8, w.batch, int(lens.max())) as attn:
-        args = (up_bf16(q), k, v, up_i32(lay.offsets), up_i32(lens), up_i32(q_starts), up_i32(nq), int(nq.max()), w.scale)
-        attn.prefill(*args, out)
-        attn.prefill(*args, out_split, split_p=True)
-        torch.cuda.synchronize()
-    seqs = [int(np.argmax(lens)), int(np.argmin(lens)), 3, 100]
-    hk, hv, sub_offs, sub_lens, rows = [], [], [], [], []
-    base = 0
-    for b in seqs:
-        o, L = int(lay.offsets[b]), int(lens[b])
-        hk.append(k[o:o + L].view(torch.int16).cpu().numpy().view(np.uint16))
-        hv.append(v[o:o + L].view(torch.int16).cpu().numpy().view(np.uint16))
-        for i in sorted(set([0, int(nq[b]) - 1] + list(rng.integers(0, nq[b], size=6)))):
-            rows.append(q_starts[b] + i)
-            sub_offs.append(base)
-            sub_lens.append(L - int(nq[b]) + i + 1)
-        base += L
-    hk, hv = np.concatenate(hk), np.concatenate(hv)
-    ref = oracle.decode_attn(q[rows], hk, hv, np.array(sub_offs), np.array(sub_lens), w.scale)
-    assert_parity(out.cpu().numpy()[rows], ref, f"prefill act-first burst, {len(rows)} sampled rows", tight=False)
-    assert_parity(out_split.cpu().numpy()[rows], ref, "same, two-term weights")
-    assert np.isfinite(out.cpu().numpy()).all() and np.isfinite(out_split.cpu().numpy()).all()
-
-
 def test_prefill_abi():
     lib = bd.load_library()
     with DecodeAttention(32, 8, 2, 32) as attn:
