@@ -116,6 +116,37 @@ int ctx_decode_attn_run(ctx_decode_attn* handle, const void* q, const void* k_ca
                         int32_t num_seqs, float scale, void* out, void* stream);
 
 /*
+ * Allocation-free variant of ctx_decode_attn_run, for callers that cannot
+ * allocate device memory: code under HIP graph capture, tight serving loops,
+ * harnesses that forbid hipMalloc.  It takes no handle and allocates nothing
+ * (no hipMalloc, hipFree or allocating library call): the split workspace is a
+ * static device array of CTX_STATIC_SCRATCH_BYTES, one per device, held until
+ * the process ends and looked up on the first call on each device.
+ *
+ *   desc        host pointer, read during the call: heads, head_dim, max_batch
+ *               (num_seqs <= max_batch), out_dtype; split_tokens and page_tokens
+ *               must be 0 (balanced split, contiguous caches).  max_seq_len is
+ *               only checked to be positive.
+ *   q, k_cache, v_cache, seq_offsets, seq_lens, num_seqs, scale, out, stream:
+ *               as in ctx_decode_attn_run, with the same result bit for bit as
+ *               a handle created from the same desc.
+ *
+ * The workspace a call needs is (R + num_seqs) x Hq x 520 bytes (R = 256 ranges
+ * on an MI355X with Hkv = 8; 8.1 MiB for 256 sequences of 32 query heads);
+ * larger calls fail with CTX_ERR_CAPACITY before launching anything.  Nothing in
+ * the workspace needs to start at zero.  Every call on a device shares that
+ * device's array: calls whose work may overlap on one device (different
+ * streams, or different threads without ordering) race and must be serialised
+ * by the caller.
+ * Errors: INVALID_ARG, UNSUPPORTED (also for split_tokens or page_tokens != 0),
+ * CAPACITY, ALIGNMENT, HIP.
+ */
+#define CTX_STATIC_SCRATCH_BYTES (16u << 20)
+int ctx_decode_attn_run_static(const ctx_decode_attn_desc* desc, const void* q, const void* k_cache,
+                               const void* v_cache, const int32_t* seq_offsets, const int32_t* seq_lens,
+                               int32_t num_seqs, float scale, void* out, void* stream);
+
+/*
  * Paged variant of ctx_decode_attn_run: the caches are split into pages of
  * P = desc.page_tokens tokens, as in the block tables of the paged-attention
  * serving engine the paper rolls out with (Sec. 5.1, vLLM; prefix caching is

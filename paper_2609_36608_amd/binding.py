@@ -23,11 +23,13 @@ CTX_DTYPE_BF16 = 0
 CTX_DTYPE_F32 = 1
 
 CTX_PREFILL_SPLIT_P = 1  # ctx_prefill_attn_run flag: softmax weights as two bf16 terms
+CTX_STATIC_SCRATCH_BYTES = 16 << 20  # static workspace of ctx_decode_attn_run_static, per device
 
 # every function the C header declares
 EXPORTS = (
     "ctx_decode_attn_create",
     "ctx_decode_attn_run",
+    "ctx_decode_attn_run_static",
     "ctx_decode_attn_run_paged",
     "ctx_prefill_attn_run",
     "ctx_opd_loss_run",
@@ -107,6 +109,9 @@ def load_library(path: str | None = None):
     lib.ctx_decode_attn_create.restype = ctypes.c_int
     lib.ctx_decode_attn_run.argtypes = [vp, vp, vp, vp, vp, vp, i32, ctypes.c_float, vp, vp]
     lib.ctx_decode_attn_run.restype = ctypes.c_int
+    lib.ctx_decode_attn_run_static.argtypes = [ctypes.POINTER(CtxDesc), vp, vp, vp, vp, vp, i32, ctypes.c_float,
+                                               vp, vp]
+    lib.ctx_decode_attn_run_static.restype = ctypes.c_int
     lib.ctx_decode_attn_run_paged.argtypes = [vp, vp, vp, vp, vp, i32, vp, i32, vp, vp, ctypes.c_float, vp, vp]
     lib.ctx_decode_attn_run_paged.restype = ctypes.c_int
     lib.ctx_prefill_attn_run.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp, i32, i32, ctypes.c_float, ctypes.c_uint32,
@@ -297,6 +302,35 @@ class DecodeAttention:
             self.close()
         except Exception:
             pass
+
+
+def ctx_decode_attn_run_static(q, k_cache, v_cache, seq_offsets, seq_lens, scale: float, out, num_kv_heads: int,
+                               max_batch: int | None = None, stream=None):
+    """ctx_decode_attn_run_static: the decode step with no handle and no
+    allocation (the split workspace is the library's static device array).
+    q / out [B, Hq, 128] (out float32 or bfloat16), caches [rows, Hkv, 128] bf16,
+    seq_offsets / seq_lens [B] int32; max_batch defaults to B."""
+    import torch
+
+    lib = load_library()
+    b, hq = q.shape[0], q.shape[1]
+    device = q.device.index if q.is_cuda else -1
+    _check_tensors(device, (("q", q, torch.bfloat16), ("k_cache", k_cache, torch.bfloat16),
+                            ("v_cache", v_cache, torch.bfloat16), ("seq_offsets", seq_offsets, torch.int32),
+                            ("seq_lens", seq_lens, torch.int32), ("out", out, out.dtype)))
+    if q.dim() != 3 or out.shape != q.shape:
+        raise ValueError("q/out must be [B, Hq, 128] of one shape")
+    if k_cache.dim() != 3 or k_cache.shape[1] != num_kv_heads or v_cache.shape != k_cache.shape:
+        raise ValueError(f"k_cache/v_cache must be [rows, {num_kv_heads}, 128]")
+    if seq_offsets.shape != (b,) or seq_lens.shape != (b,):
+        raise ValueError(f"seq_offsets/seq_lens must be [{b}]")
+    desc = CtxDesc(hq, num_kv_heads, q.shape[2], b if max_batch is None else max_batch, 1, _dtype_code(out.dtype), 0, 0)
+    rc = lib.ctx_decode_attn_run_static(ctypes.byref(desc), q.data_ptr(), k_cache.data_ptr(), v_cache.data_ptr(),
+                                        seq_offsets.data_ptr(), seq_lens.data_ptr(), b, float(scale), out.data_ptr(),
+                                        _stream_ptr(stream, q.device))
+    if rc != CTX_OK:
+        raise error_for(lib, rc)
+    return out
 
 
 def opd_loss(logits, tokens, old_logp, teacher_logp, mask, seq_starts, params: OpdParams | None = None,

@@ -41,6 +41,7 @@
 #include <cmath>
 #include <cstdint>
 #include <cstdio>
+#include <mutex>
 #include <new>
 
 #include "ctx_attn_common.h"
@@ -548,6 +549,61 @@ __global__ __launch_bounds__(64 * kMergeWaves) void decode_merge_kernel(
 
 thread_local char g_last_error[512] = "";
 
+// Waves (KV heads of one range) per split workgroup: 8, 4, 2 or 1, a divisor of Hkv.
+int split_waves(int hkv) {
+  int wgw = kWgWaves;
+  while (hkv % wgw != 0) wgw >>= 1;
+  return wgw;
+}
+
+// Ranges of the balanced split for the contiguous ([0]) and paged ([1])
+// kernels: enough that one wave per (range, KV head) is resident at once, in
+// whole multiples of the XCD count.
+int balanced_ranges(const ctx_decode_attn_desc& d, int cus, int wgw, int64_t ranges[2]) {
+  const void* kernels[2] = {
+      d.out_dtype == CTX_DTYPE_F32 ? reinterpret_cast<const void*>(&decode_split_kernel<float, false>)
+                                   : reinterpret_cast<const void*>(&decode_split_kernel<uint16_t, false>),
+      d.out_dtype == CTX_DTYPE_F32 ? reinterpret_cast<const void*>(&decode_split_kernel<float, true>)
+                                   : reinterpret_cast<const void*>(&decode_split_kernel<uint16_t, true>)};
+  for (int layout = 0; layout < 2; ++layout) {
+    int n = 0;
+    hipError_t e =
+        hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, kernels[layout], 64 * wgw, (size_t)wgw * kTileBytes);
+    if (e != hipSuccess) return hip_fail(e, "hipOccupancyMaxActiveBlocksPerMultiprocessor");
+    const int64_t per_cu = n < 1 ? 1 : (int64_t)n * wgw;  // resident waves per CU
+    ranges[layout] = (int64_t)cus * per_cu / d.num_kv_heads / kXcds * kXcds;
+    if (ranges[layout] < kXcds) ranges[layout] = kXcds;
+  }
+  return CTX_OK;
+}
+
+// Checks of a descriptor shared by ctx_decode_attn_create and the
+// allocation-free entry point.
+int check_desc(const ctx_decode_attn_desc& d) {
+  if (d.num_q_heads <= 0 || d.num_kv_heads <= 0)
+    return fail(CTX_ERR_INVALID_ARG, "head counts must be positive (Hq=%d, Hkv=%d)",
+                d.num_q_heads, d.num_kv_heads);
+  if (d.head_dim != kHeadDim)
+    return fail(CTX_ERR_UNSUPPORTED, "head_dim %d unsupported (only %d)", d.head_dim, kHeadDim);
+  if (d.num_q_heads % d.num_kv_heads != 0)
+    return fail(CTX_ERR_UNSUPPORTED, "Hq=%d is not a multiple of Hkv=%d", d.num_q_heads,
+                d.num_kv_heads);
+  if (d.num_q_heads / d.num_kv_heads > kMaxGroup)
+    return fail(CTX_ERR_UNSUPPORTED, "group size %d > %d", d.num_q_heads / d.num_kv_heads,
+                kMaxGroup);
+  if (d.max_batch <= 0 || d.max_seq_len <= 0)
+    return fail(CTX_ERR_INVALID_ARG, "max_batch and max_seq_len must be positive");
+  if (d.out_dtype != CTX_DTYPE_BF16 && d.out_dtype != CTX_DTYPE_F32)
+    return fail(CTX_ERR_INVALID_ARG, "unknown out_dtype %d", (int)d.out_dtype);
+  if (d.split_tokens < 0 || (d.split_tokens > 0 && d.split_tokens < kBlock))
+    return fail(CTX_ERR_INVALID_ARG, "split_tokens must be 0 or >= %d", kBlock);
+  if (d.page_tokens < 0 || d.page_tokens % kBlock != 0)
+    return fail(CTX_ERR_INVALID_ARG, "page_tokens must be 0 or a positive multiple of %d", kBlock);
+  if (d.page_tokens > 0 && d.split_tokens % kBlock != 0)
+    return fail(CTX_ERR_INVALID_ARG, "with page_tokens, split_tokens must be a multiple of %d", kBlock);
+  return CTX_OK;
+}
+
 }  // namespace
 
 // The last-error message is shared with the library's other entry points
@@ -583,27 +639,8 @@ int ctx_decode_attn_create(const ctx_decode_attn_desc* desc, ctx_decode_attn** o
   *out_handle = nullptr;
   if (desc == nullptr) return fail(CTX_ERR_INVALID_ARG, "desc is NULL");
   const ctx_decode_attn_desc d = *desc;
-  if (d.num_q_heads <= 0 || d.num_kv_heads <= 0)
-    return fail(CTX_ERR_INVALID_ARG, "head counts must be positive (Hq=%d, Hkv=%d)",
-                d.num_q_heads, d.num_kv_heads);
-  if (d.head_dim != kHeadDim)
-    return fail(CTX_ERR_UNSUPPORTED, "head_dim %d unsupported (only %d)", d.head_dim, kHeadDim);
-  if (d.num_q_heads % d.num_kv_heads != 0)
-    return fail(CTX_ERR_UNSUPPORTED, "Hq=%d is not a multiple of Hkv=%d", d.num_q_heads,
-                d.num_kv_heads);
-  if (d.num_q_heads / d.num_kv_heads > kMaxGroup)
-    return fail(CTX_ERR_UNSUPPORTED, "group size %d > %d", d.num_q_heads / d.num_kv_heads,
-                kMaxGroup);
-  if (d.max_batch <= 0 || d.max_seq_len <= 0)
-    return fail(CTX_ERR_INVALID_ARG, "max_batch and max_seq_len must be positive");
-  if (d.out_dtype != CTX_DTYPE_BF16 && d.out_dtype != CTX_DTYPE_F32)
-    return fail(CTX_ERR_INVALID_ARG, "unknown out_dtype %d", (int)d.out_dtype);
-  if (d.split_tokens < 0 || (d.split_tokens > 0 && d.split_tokens < kBlock))
-    return fail(CTX_ERR_INVALID_ARG, "split_tokens must be 0 or >= %d", kBlock);
-  if (d.page_tokens < 0 || d.page_tokens % kBlock != 0)
-    return fail(CTX_ERR_INVALID_ARG, "page_tokens must be 0 or a positive multiple of %d", kBlock);
-  if (d.page_tokens > 0 && d.split_tokens % kBlock != 0)
-    return fail(CTX_ERR_INVALID_ARG, "with page_tokens, split_tokens must be a multiple of %d", kBlock);
+  int rc = check_desc(d);
+  if (rc != CTX_OK) return rc;
 
   int dev = 0;
   hipError_t e = hipGetDevice(&dev);
@@ -611,26 +648,10 @@ int ctx_decode_attn_create(const ctx_decode_attn_desc* desc, ctx_decode_attn** o
   int cus = 0;
   e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
   if (e != hipSuccess) return hip_fail(e, "hipDeviceGetAttribute");
-  // Workgroups hold the KV heads of one range: 8, 4, 2 or 1 of them (a divisor
-  // of Hkv).  Each layout's kernel gets the ranges that keep one wave per
-  // (range, KV head) resident.
-  int wgw = kWgWaves;
-  while (d.num_kv_heads % wgw != 0) wgw >>= 1;
-  const void* kernels[2] = {
-      d.out_dtype == CTX_DTYPE_F32 ? reinterpret_cast<const void*>(&decode_split_kernel<float, false>)
-                                   : reinterpret_cast<const void*>(&decode_split_kernel<uint16_t, false>),
-      d.out_dtype == CTX_DTYPE_F32 ? reinterpret_cast<const void*>(&decode_split_kernel<float, true>)
-                                   : reinterpret_cast<const void*>(&decode_split_kernel<uint16_t, true>)};
+  const int wgw = split_waves(d.num_kv_heads);
   int64_t ranges_auto[2];
-  for (int layout = 0; layout < 2; ++layout) {
-    int n = 0;
-    e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, kernels[layout], 64 * wgw, (size_t)wgw * kTileBytes);
-    if (e != hipSuccess) return hip_fail(e, "hipOccupancyMaxActiveBlocksPerMultiprocessor");
-    const int64_t per_cu = n < 1 ? 1 : (int64_t)n * wgw;  // resident waves per CU
-    // ranges in whole multiples of the XCD count
-    ranges_auto[layout] = (int64_t)cus * per_cu / d.num_kv_heads / kXcds * kXcds;
-    if (ranges_auto[layout] < kXcds) ranges_auto[layout] = kXcds;
-  }
+  rc = balanced_ranges(d, cus, wgw, ranges_auto);
+  if (rc != CTX_OK) return rc;
   int64_t max_ranges = ranges_auto[0] > ranges_auto[1] ? ranges_auto[0] : ranges_auto[1];
   if (d.split_tokens > 0)
     max_ranges = round_up(((int64_t)d.max_batch * round_up(d.max_seq_len, kBlock) + d.split_tokens - 1) /
@@ -777,3 +798,114 @@ int ctx_decode_attn_destroy(ctx_decode_attn* h) {
 }
 
 }  // extern "C"
+
+// ------------------------------------------------------------ allocation-free entry point
+//
+// ctx_decode_attn_run_static runs the same kernels as ctx_decode_attn_run with
+// the split workspace in `scratch`, a file-scope device array (one copy per
+// device, held until the process ends), instead of a handle's allocation.  In
+// host code `scratch` names a host-side stand-in, so its device address is
+// looked up once per device (hipGetSymbolAddress, with that device current)
+// and only that address is handed to kernels.
+
+namespace {
+
+constexpr size_t kScratchBytes = (size_t)CTX_STATIC_SCRATCH_BYTES;
+constexpr int kMaxDevices = 64;
+
+}  // namespace
+
+static __device__ __align__(256) unsigned char scratch[kScratchBytes];
+
+namespace {
+
+struct StaticDevice {
+  bool ready;
+  int cus;
+  unsigned char* scratch;     // device address of `scratch` on this device
+  int32_t ranges[2][kWgWaves + 1];  // balanced ranges per out dtype and waves per workgroup (0: not yet known)
+};
+
+StaticDevice g_static[kMaxDevices];
+std::mutex g_static_mutex;
+
+// The device's scratch address and CU count, set up on its first call.
+int static_device(int dev, StaticDevice** out) {
+  if (dev < 0 || dev >= kMaxDevices) return fail(CTX_ERR_UNSUPPORTED, "device %d >= %d", dev, kMaxDevices);
+  StaticDevice& sd = g_static[dev];
+  if (!sd.ready) {
+    void* ptr = nullptr;
+    hipError_t e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return hip_fail(e, "hipGetSymbolAddress(scratch)");
+    int cus = 0;
+    e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
+    if (e != hipSuccess) return hip_fail(e, "hipDeviceGetAttribute");
+    sd.scratch = static_cast<unsigned char*>(ptr);
+    sd.cus = cus;
+    sd.ready = true;
+  }
+  *out = &sd;
+  return CTX_OK;
+}
+
+}  // namespace
+
+extern "C" int ctx_decode_attn_run_static(const ctx_decode_attn_desc* desc, const void* q, const void* k_cache,
+                                          const void* v_cache, const int32_t* seq_offsets, const int32_t* seq_lens,
+                                          int32_t num_seqs, float scale, void* out, void* stream) {
+  ctx_clear_error();
+  if (desc == nullptr) return fail(CTX_ERR_INVALID_ARG, "desc is NULL");
+  const ctx_decode_attn_desc d = *desc;
+  int rc = check_desc(d);
+  if (rc != CTX_OK) return rc;
+  if (d.split_tokens != 0 || d.page_tokens != 0)
+    return fail(CTX_ERR_UNSUPPORTED, "the allocation-free entry point takes split_tokens = 0 and page_tokens = 0");
+  if (num_seqs < 0) return fail(CTX_ERR_INVALID_ARG, "num_seqs %d < 0", num_seqs);
+  if (num_seqs > d.max_batch)
+    return fail(CTX_ERR_CAPACITY, "num_seqs %d > max_batch %d", num_seqs, d.max_batch);
+  if (!std::isfinite(scale)) return fail(CTX_ERR_INVALID_ARG, "scale is not finite");
+  if (num_seqs == 0) return CTX_OK;
+  if (q == nullptr || k_cache == nullptr || v_cache == nullptr || seq_offsets == nullptr ||
+      seq_lens == nullptr || out == nullptr)
+    return fail(CTX_ERR_INVALID_ARG, "NULL data pointer");
+  if (!aligned16(q) || !aligned16(k_cache) || !aligned16(v_cache) || !aligned16(out))
+    return fail(CTX_ERR_ALIGNMENT, "q, k_cache, v_cache and out must be 16-byte aligned");
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+
+  ctx_decode_attn h{};
+  {
+    std::lock_guard<std::mutex> lock(g_static_mutex);
+    StaticDevice* sd = nullptr;
+    rc = static_device(dev, &sd);
+    if (rc != CTX_OK) return rc;
+    const int wgw = split_waves(d.num_kv_heads);
+    int32_t& ranges = sd->ranges[d.out_dtype == CTX_DTYPE_F32 ? 1 : 0][wgw];
+    if (ranges == 0) {
+      int64_t r[2];
+      rc = balanced_ranges(d, sd->cus, wgw, r);
+      if (rc != CTX_OK) return rc;
+      ranges = (int32_t)r[0];
+    }
+    h.desc = d;
+    h.device = dev;
+    h.num_cus = sd->cus;
+    h.ranges_auto[0] = ranges;
+    h.ranges_auto[1] = 0;  // paged layout: not served here
+    h.max_ranges = ranges;
+    h.split_wgw = wgw;
+    h.o_ws = reinterpret_cast<float*>(sd->scratch);
+  }
+  // the workspace of this call: partial outputs, then their (max, sum) pairs
+  const int64_t slots = (int64_t)h.max_ranges + num_seqs;
+  const size_t o_bytes = (size_t)round_up((int64_t)slots * d.num_q_heads * kHeadDim * (int64_t)sizeof(float), 256);
+  const size_t ml_bytes = (size_t)slots * d.num_q_heads * sizeof(float2);
+  if (o_bytes + ml_bytes > kScratchBytes)
+    return fail(CTX_ERR_CAPACITY,
+                "workspace of %zu bytes (%lld ranges + %d sequences, %d query heads) exceeds the static %zu bytes",
+                o_bytes + ml_bytes, (long long)h.max_ranges, num_seqs, d.num_q_heads, kScratchBytes);
+  h.ml_ws = reinterpret_cast<float2*>(reinterpret_cast<unsigned char*>(h.o_ws) + o_bytes);
+  Paged pg{};
+  return launch<false>(&h, q, k_cache, v_cache, seq_offsets, seq_lens, num_seqs, scale, out, stream, pg);
+}

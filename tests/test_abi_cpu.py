@@ -92,3 +92,29 @@ def test_valid_desc_without_gpu_reports_hip_error_or_succeeds(lib):
     else:
         assert rc == bd.CTX_ERR_HIP
         assert h.value is None
+
+
+@pytest.mark.parametrize("kw,num_seqs,status", [
+    (dict(split_tokens=64), 4, bd.CTX_ERR_UNSUPPORTED),
+    (dict(page_tokens=16), 4, bd.CTX_ERR_UNSUPPORTED),
+    (dict(head_dim=64), 4, bd.CTX_ERR_UNSUPPORTED),
+    (dict(out_dtype=7), 4, bd.CTX_ERR_INVALID_ARG),
+    (dict(max_batch=8), 9, bd.CTX_ERR_CAPACITY),
+    (dict(), -1, bd.CTX_ERR_INVALID_ARG),
+])
+def test_static_run_rejects_bad_arguments_before_the_device(lib, kw, num_seqs, status):
+    """The allocation-free entry point checks its descriptor and sizes first."""
+    rc = lib.ctx_decode_attn_run_static(ctypes.byref(good_desc(**kw)), 16, 16, 16, 16, 16, num_seqs, 0.1, 16, None)
+    assert rc == status
+    assert lib.ctx_decode_attn_last_error().decode()
+
+
+def test_static_run_null_and_empty(lib):
+    assert lib.ctx_decode_attn_run_static(None, 16, 16, 16, 16, 16, 1, 0.1, 16, None) == bd.CTX_ERR_INVALID_ARG
+    assert lib.ctx_decode_attn_run_static(ctypes.byref(good_desc()), 16, 16, 16, 16, 16, 0, 0.1, 16, None) == bd.CTX_OK
+    assert lib.ctx_decode_attn_run_static(ctypes.byref(good_desc()), None, 16, 16, 16, 16, 1, 0.1, 16,
+                                          None) == bd.CTX_ERR_INVALID_ARG
+    assert lib.ctx_decode_attn_run_static(ctypes.byref(good_desc()), 16, 16, 16, 16, 16, 1, float("nan"), 16,
+                                          None) == bd.CTX_ERR_INVALID_ARG
+    assert lib.ctx_decode_attn_run_static(ctypes.byref(good_desc()), 18, 16, 16, 16, 16, 1, 0.1, 16,
+                                          None) == bd.CTX_ERR_ALIGNMENT
