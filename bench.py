@@ -141,6 +141,72 @@ def cpu_model() -> str:
     return ""
 
 
+def read_ceiling(torch, dev, achieved_gbs: float) -> dict:
+    """The device's streaming-read rate (ctx_hbm_read: non-temporal 16-byte
+    loads over 4 GiB, median of 8 launches), measured in this process, and the
+    fraction of it that `achieved_gbs` reaches."""
+    from paper_2609_36608_amd import rollout_calibration as rcal
+
+    r = rcal.measure_hbm(torch, dev, gib=4.0, reps=8)
+    return {"read_gbs": r["gbs"], "best_gbs": r["best_gbs"], "frac": round(achieved_gbs / r["gbs"], 4),
+            "source": f"ctx_hbm_read, 4 GiB, {r['workgroups']} workgroups, median of {r['reps']} in this process"}
+
+
+def copy_ceiling(torch, dev, achieved_gbs: float) -> dict:
+    """The device's 1:1 read/write streaming rate (ctx_hbm_copy over 4 GiB,
+    bytes read plus written, median of 8 launches) in this process."""
+    from paper_2609_36608_amd import rollout_calibration as rcal
+
+    r = rcal.measure_hbm(torch, dev, gib=4.0, reps=8, copy=True)
+    return {"copy_gbs": r["gbs"], "best_gbs": r["best_gbs"], "frac": round(achieved_gbs / r["gbs"], 4),
+            "source": f"ctx_hbm_copy, 4 GiB read + 4 GiB written, {r['workgroups']} workgroups, "
+                      f"median of {r['reps']} in this process"}
+
+
+CEILING_METRIC = "HBM streaming ceiling GB/s (fraction of 8 TB/s peak), 1 MI355X"
+
+
+def bench_ceiling(args) -> int:
+    """Read-only and 1:1 read/write streaming kernels of the library
+    (ctx_hbm_read, ctx_hbm_copy) over 8 GiB, each launched --steps times."""
+    import torch
+
+    from paper_2609_36608_amd import rollout_calibration as rcal
+
+    if not torch.cuda.is_available():
+        print("bench.py: no GPU visible", file=sys.stderr)
+        return 1
+    dev = torch.device("cuda", 0)
+    torch.cuda.set_device(dev)
+    res = {}
+    for name, copy, nt in (("read_nt", False, True), ("read_cached", False, False), ("copy_nt", True, True),
+                           ("copy_cached", True, False)):
+        res[name] = rcal.measure_hbm(torch, dev, gib=8.0, reps=args.steps, copy=copy, nontemporal=nt)
+    best = res["read_nt"]
+    result = {
+        "metric": CEILING_METRIC,
+        "value": best["gbs"],
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": 1,
+        "ms_per_step": round(best["bytes"] / best["gbs"] / 1e6, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "u8",
+        "data": "synthetic",
+        "config": {"workload": "8 GiB buffer streamed once per launch (copy: 8 GiB read + 8 GiB written)",
+                   "parallelism": "none (1 GPU)"},
+        "frac_of_hbm_peak": round(best["gbs"] / HBM_PEAK_GBS, 4),
+        "kernels": {k: {kk: v[kk] for kk in ("gbs", "best_gbs", "workgroups", "nontemporal", "kernel")}
+                    for k, v in res.items()},
+        "device": device_info(torch, dev),
+    }
+    print(json.dumps(result), flush=True)
+    return 0
+
+
 PREFILL_METRIC = "causal prefill attention TFLOP/s (fraction of 2.5 PFLOP/s bf16 MFMA peak), 1 MI355X"
 MFMA_BF16_PEAK_TFLOPS = 2500.0
 
@@ -451,6 +517,7 @@ def bench_opd(args) -> int:
             "peak": HBM_PEAK_GBS,
             "unit": "GB/s",
             "frac": round(gbs / HBM_PEAK_GBS, 4),
+            "ceiling": copy_ceiling(torch, dev, gbs),
             **traffic_fields(w.name, "opd_row_kernel"),
             "kernel": "opd_row_kernel (+ opd_weight_kernel, opd_reduce_kernel: one ctx_opd_loss_run call)",
             "bytes_per_launch": nbytes,
@@ -468,54 +535,7 @@ def bench_opd(args) -> int:
 
 SIM_METRIC = ("simulated rollout speedup, ActFirst-OPD over think-then-act (16 tasks, T=30, b_max=256, "
               "16-token fast actions, 512-token full responses), engine model with MI355X-measured attention cost")
-# Qwen3-1.7B, the student of the rollout-efficiency study: 28 layers, 16 query
-# and 8 KV heads of 128; about 1.72e9 bf16 parameters streamed once per decode step
-SIM_LAYERS, SIM_HQ, SIM_HKV, SIM_PARAMS = 28, 16, 8, 1.72e9
-COPY_CEILING_GBS = 7090.0   # measured streaming-read ceiling of this part (NT loads)
-
-
-def calibrate_attention(torch, dev):
-    """Time ctx_decode_attn_run at the Qwen3-1.7B shape for several batches and
-    context lengths; least-squares fit of seconds per call = a + b * KV tokens."""
-    from paper_2609_36608_amd.binding import DecodeAttention
-
-    pts = []
-    total_bytes, total_s = 0, 0.0
-    for batch, ctx in [(16, 2048), (64, 2048), (64, 4096), (128, 3072), (256, 2048), (256, 4096)]:
-        lens = np.full(batch, ctx, np.int32)
-        layout = wl.make_layout(lens, 1)
-        k = torch.empty((layout.num_rows, SIM_HKV, 128), dtype=torch.bfloat16, device=dev)
-        v = torch.empty_like(k)
-        wl.fill_normal_bf16_device(k, 7, batch, ctx, 1)
-        wl.fill_normal_bf16_device(v, 7, batch, ctx, 2)
-        q = torch.empty((batch, SIM_HQ, 128), dtype=torch.bfloat16, device=dev)
-        wl.fill_normal_bf16_device(q, 7, batch, ctx, 0)
-        out = torch.empty((batch, SIM_HQ, 128), dtype=torch.float32, device=dev)
-        offs = torch.from_numpy(layout.offsets).to(dev)
-        tl = torch.from_numpy(lens).to(dev)
-        with DecodeAttention(SIM_HQ, SIM_HKV, batch, ctx) as attn:
-            for _ in range(3):
-                attn.run(q, k, v, offs, tl, 0.0884, out)
-            torch.cuda.synchronize()
-            reps = 50
-            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-            e0.record()
-            for _ in range(reps):
-                attn.run(q, k, v, offs, tl, 0.0884, out)
-            e1.record()
-            e1.synchronize()
-            sec = e0.elapsed_time(e1) / 1e3 / reps
-        pts.append((batch * ctx, sec))
-        w = wl.Workload("sim", 0, 1, batch, SIM_HQ, SIM_HKV, 1, "uniform", ctx, ctx)
-        total_bytes += algorithmic_bytes(lens, w) * reps
-        total_s += sec * reps
-        del k, v
-    x = np.array([p[0] for p in pts], np.float64)
-    y = np.array([p[1] for p in pts], np.float64)
-    b, a = np.polyfit(x, y, 1)
-    return {"per_call_s": float(a), "per_kv_token_s": float(b), "points": pts,
-            "achieved_gbs": total_bytes / total_s / 1e9, "avg_call_us": total_s / (len(pts) * 50) * 1e6,
-            "bytes_per_call": total_bytes / (len(pts) * 50)}
+SIM_CALIBRATIONS = 3  # independent calibrations; the headline is reported for each
 
 
 def sim_contexts(n: int, turns: int, seed: int = wl.DEFAULT_SEED) -> np.ndarray:
@@ -526,37 +546,40 @@ def sim_contexts(n: int, turns: int, seed: int = wl.DEFAULT_SEED) -> np.ndarray:
 
 
 def bench_sim(args) -> int:
-    """Calibrate the decode-step cost on the GPU, then run the rollout scans of
-    the rollout-efficiency study through the native engine-model simulator."""
+    """Calibrate the engine model on the GPU (decode attention cost, read
+    ceiling, prefill rate; all measured in this process), SIM_CALIBRATIONS
+    times, then run the rollout scans of the rollout-efficiency study through
+    the native engine-model simulator with each calibration."""
     import torch
 
     from paper_2609_36608_amd import binding
+    from paper_2609_36608_amd import rollout_calibration as rcal
 
     if not torch.cuda.is_available():
         print("bench.py: no GPU visible", file=sys.stderr)
         return 1
     dev = torch.device("cuda", 0)
     torch.cuda.set_device(dev)
-    cal = calibrate_attention(torch, dev)
-    weight_s = SIM_PARAMS * 2 / (COPY_CEILING_GBS * 1e9)
-    eng = dict(step_base=weight_s + SIM_LAYERS * cal["per_call_s"],
-               step_per_kv_token=SIM_LAYERS * cal["per_kv_token_s"],
-               prefill_per_token=2 * SIM_PARAMS / 680e12)
+    cals = [rcal.calibrate_engine(torch, dev) for _ in range(SIM_CALIBRATIONS)]
     n = 16
 
-    def speedup(turns, b_max, full_tokens):
+    def speedup(eng, turns, b_max, full_tokens):
         ctx = sim_contexts(n, turns)
         v = binding.rollout_simulate_engine(binding.ROLLOUT_VANILLA, ctx, 16, full_tokens, b_max, **eng)
         a = binding.rollout_simulate_engine(binding.ROLLOUT_ACTFIRST, ctx, 16, full_tokens, b_max, **eng)
         return v["completion"] / a["completion"], v, a
 
+    heads = [speedup(c["engine"], 30, 256, 512)[0] for c in cals]
+    cal = cals[int(np.argsort(heads)[len(heads) // 2])]  # the median calibration drives the scans
+    eng = cal["engine"]
     t0 = time.perf_counter()
-    conc = {ft: {b: round(speedup(30, b, ft)[0], 3) for b in (16, 32, 64, 128, 256)} for ft in (128, 512)}
-    hor = {ft: {t: round(speedup(t, 256, ft)[0], 3) for t in (1, 2, 4, 8, 16, 30)} for ft in (128, 512)}
-    head, v, a = speedup(30, 256, 512)
+    conc = {ft: {b: round(speedup(eng, 30, b, ft)[0], 3) for b in (16, 32, 64, 128, 256)} for ft in (128, 512)}
+    hor = {ft: {t: round(speedup(eng, t, 256, ft)[0], 3) for t in (1, 2, 4, 8, 16, 30)} for ft in (128, 512)}
+    head, v, a = speedup(eng, 30, 256, 512)
     native_s = time.perf_counter() - t0
     nsim = 2 * (5 + 6) * 2 + 2
     requests = 2 * n * 30
+    att = cal["attention"]
     result = {
         "metric": SIM_METRIC,
         "value": round(head, 4),
@@ -574,12 +597,15 @@ def bench_sim(args) -> int:
             "workload": "rollout-efficiency scans: 16 tasks, fixed contexts U{1500..3000} tokens, 16-token fast "
                         "actions, 128- or 512-token full responses; b_max scan at T=30, T scan at b_max=256",
             "engine": {k: float(f"{x:.6g}") for k, x in eng.items()},
-            "engine_sources": "step_per_kv_token and the per-layer call cost: ctx_decode_attn_run timed on this GPU "
-                              "at 28 layers, 16/8 heads; step weight streaming: 1.72e9 bf16 parameters at the measured "
-                              "7.09 TB/s read ceiling; prefill: 2 x parameters flops per token at the measured "
-                              "prefill-kernel rate (680 TFLOP/s)",
+            "engine_sources": cal["sources"],
             "parallelism": "none (1 GPU)",
         },
+        "calibrations": [{"speedup": round(h, 4), "engine": {k: float(f"{x:.6g}") for k, x in c["engine"].items()},
+                          "read_ceiling_gbs": c["read_ceiling"]["gbs"],
+                          "prefill_tflops": round(c["prefill"]["tflops"], 1),
+                          "attention_gbs": round(c["attention"]["achieved_gbs"], 1)} for h, c in zip(heads, cals)],
+        "speedup_spread": {"min": round(min(heads), 4), "median": round(float(np.median(heads)), 4),
+                           "max": round(max(heads), 4)},
         "speedup_vs_b_max_T30": conc,
         "speedup_vs_T_b_max256": hor,
         "paper_measured_A100_vllm": {"b_max16_to_256_128tok": [0.80, 1.49], "b_max16_to_256_512tok": [0.92, 2.42]},
@@ -588,14 +614,16 @@ def bench_sim(args) -> int:
         "requests_per_s": round(nsim * requests / native_s, 1),
         "roofline": {
             "bound": "hbm",
-            "achieved": round(cal["achieved_gbs"], 2),
+            "achieved": round(att["achieved_gbs"], 2),
             "peak": HBM_PEAK_GBS,
             "unit": "GB/s",
-            "frac": round(cal["achieved_gbs"] / HBM_PEAK_GBS, 4),
+            "frac": round(att["achieved_gbs"] / HBM_PEAK_GBS, 4),
+            "ceiling": {"read_gbs": cal["read_ceiling"]["gbs"], "source": "ctx_hbm_read in this process"},
             "traffic": None,
-            "kernel": "ctx_decode_attn_run calls of the calibration (28-layer Qwen3-1.7B shape, batches 16..256)",
-            "bytes_per_launch": round(cal["bytes_per_call"]),
-            "avg_launch_us": round(cal["avg_call_us"], 3),
+            "kernel": ("ctx_decode_attn_run calls of the calibration (Qwen3-1.7B shape, 16/8 heads, batches 16..256, "
+                       "distinct caches of >= 1 GiB in rotation per point)"),
+            "bytes_per_launch": round(att["bytes_per_call"]),
+            "avg_launch_us": round(att["avg_call_us"], 3),
         },
     }
     if not args.no_cpu_baseline:
@@ -659,6 +687,8 @@ def main() -> int:
                     help="time the fused OPD token loss + logits gradient instead (64 responses, Qwen3 vocabulary)")
     ap.add_argument("--sim", action="store_true",
                     help="calibrate the decode-step cost on the GPU and run the rollout scheduling scans")
+    ap.add_argument("--ceiling", action="store_true",
+                    help="time the library's streaming read and copy kernels (the practical HBM ceiling) instead")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--calibrate-copy-gib", type=float, default=0.0,
@@ -680,6 +710,8 @@ def main() -> int:
         return bench_opd(args)
     if args.sim:
         return bench_sim(args)
+    if args.ceiling:
+        return bench_ceiling(args)
 
     import torch
 
@@ -828,6 +860,7 @@ def main() -> int:
         dst.copy_(src)
         torch.cuda.synchronize()
         del src, dst
+    ceiling = read_ceiling(torch, dev, per_call_bytes / call_s / 1e9)
 
     result = {
         "metric": METRIC,
@@ -867,6 +900,7 @@ def main() -> int:
             "peak": HBM_PEAK_GBS,
             "unit": "GB/s",
             "frac": round(per_call_bytes / call_s / 1e9 / HBM_PEAK_GBS, 4),
+            "ceiling": ceiling,
             **traffic_fields(w.name, f"decode_split_kernel paged {args.paged}" if args.paged else "decode_split_kernel"),
             "kernel": "one ctx_decode_attn_run call (decode_split_kernel + decode_merge_kernel)",
             "bytes_per_launch": round(per_call_bytes),

@@ -24,6 +24,8 @@ CTX_DTYPE_F32 = 1
 
 CTX_PREFILL_SPLIT_P = 1  # ctx_prefill_attn_run flag: softmax weights as two bf16 terms
 CTX_STATIC_SCRATCH_BYTES = 16 << 20  # static workspace of ctx_decode_attn_run_static, per device
+CTX_HBM_SINK_BYTES_PER_WORKGROUP = 64
+CTX_HBM_NONTEMPORAL = 1
 
 # every function the C header declares
 EXPORTS = (
@@ -35,6 +37,8 @@ EXPORTS = (
     "ctx_opd_loss_run",
     "ctx_rollout_simulate",
     "ctx_rollout_simulate_engine",
+    "ctx_hbm_read",
+    "ctx_hbm_copy",
     "ctx_decode_attn_destroy",
     "ctx_decode_attn_status_string",
     "ctx_decode_attn_last_error",
@@ -125,6 +129,10 @@ def load_library(path: str | None = None):
     lib.ctx_rollout_simulate_engine.argtypes = [ctypes.POINTER(RolloutConfig), ctypes.POINTER(RolloutEngine), vp, vp,
                                                 vp, vp, vp, vp]
     lib.ctx_rollout_simulate_engine.restype = ctypes.c_int
+    lib.ctx_hbm_read.argtypes = [vp, ctypes.c_size_t, vp, i32, ctypes.c_uint32, vp]
+    lib.ctx_hbm_read.restype = ctypes.c_int
+    lib.ctx_hbm_copy.argtypes = [vp, vp, ctypes.c_size_t, i32, ctypes.c_uint32, vp]
+    lib.ctx_hbm_copy.restype = ctypes.c_int
     lib.ctx_decode_attn_destroy.argtypes = [vp]
     lib.ctx_decode_attn_destroy.restype = ctypes.c_int
     lib.ctx_decode_attn_status_string.argtypes = [ctypes.c_int]
@@ -444,3 +452,29 @@ def rollout_simulate_engine(policy: int, context_tokens, fast_tokens: int, full_
         raise error_for(lib, rc)
     return {"completion": float(comp[0]), "start": st.reshape(n, turns, 2), "end": en.reshape(n, turns, 2),
             "peak": int(pk[0]), "steps": int(steps[0])}
+
+
+def ctx_hbm_read(src, sink, workgroups: int, nontemporal: bool = True, stream=None):
+    """Stream every byte of the contiguous CUDA tensor `src` once through the
+    compute units (ctx_hbm_read); `sink` is a CUDA tensor of at least
+    workgroups * 64 bytes."""
+    lib = load_library()
+    nbytes = src.numel() * src.element_size()
+    if not src.is_contiguous() or sink.numel() * sink.element_size() < workgroups * CTX_HBM_SINK_BYTES_PER_WORKGROUP:
+        raise ValueError("src must be contiguous and sink hold workgroups * 64 bytes")
+    rc = lib.ctx_hbm_read(src.data_ptr(), nbytes, sink.data_ptr(), int(workgroups),
+                          CTX_HBM_NONTEMPORAL if nontemporal else 0, _stream_ptr(stream, src.device))
+    if rc != CTX_OK:
+        raise error_for(lib, rc)
+
+
+def ctx_hbm_copy(src, dst, workgroups: int, nontemporal: bool = True, stream=None):
+    """dst = src (contiguous CUDA tensors of equal byte size), every byte read and written once."""
+    lib = load_library()
+    nbytes = src.numel() * src.element_size()
+    if not (src.is_contiguous() and dst.is_contiguous()) or dst.numel() * dst.element_size() != nbytes:
+        raise ValueError("src and dst must be contiguous and of equal size")
+    rc = lib.ctx_hbm_copy(src.data_ptr(), dst.data_ptr(), nbytes, int(workgroups),
+                          CTX_HBM_NONTEMPORAL if nontemporal else 0, _stream_ptr(stream, src.device))
+    if rc != CTX_OK:
+        raise error_for(lib, rc)
