@@ -101,7 +101,8 @@ int ctx_decode_attn_create(const ctx_decode_attn_desc* desc, ctx_decode_attn** o
  * Sequence b reads rows [seq_offsets[b], seq_offsets[b] + seq_lens[b]); the
  * regions may come in any order, may leave gaps between them (capacity
  * reserved for growth), and must lie inside the cache.  seq_lens[b] = 0
- * gives zeros.  Keys and values must be finite.  Device-side violations
+ * gives zeros.  Keys must be finite; a non-finite value V[r, kv, d] makes only
+ * output dimension d of the heads reading it non-finite.  Device-side violations
  * (regions outside the cache, seq_lens[b] < 0, seq_lens[b] > max_seq_len
  * with split_tokens > 0) are undefined behaviour.
  *

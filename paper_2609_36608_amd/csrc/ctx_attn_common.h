@@ -67,6 +67,13 @@ __device__ __forceinline__ s16x4 lds_read_tr16(const uint16_t* p) {
   return __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4)(p));
 }
 
+// Swizzle of the LDS K/V tiles: a tile row holds one token's 16 chunks of 8
+// dimensions, chunk ch of token t at slot ch ^ tile_swizzle(t).  Conflict-free
+// for the staging writes (16 lanes per token row), the MFMA operand reads of
+// one chunk of 16 consecutive tokens (ds_read_b128) and the transpose reads of
+// 8 tokens x 2 chunks per 32 lanes (ds_read_b64_tr_b16).
+__device__ __forceinline__ int tile_swizzle(int t) { return ((t & 7) << 1) | ((t >> 3) & 1); }
+
 // 16-byte load of data read once (non-temporal)
 __device__ __forceinline__ u32x4 load16(const uint16_t* p) {
   return __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(p));

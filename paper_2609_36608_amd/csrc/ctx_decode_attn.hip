@@ -18,13 +18,14 @@
 //   * Per 16-token block, all g query heads of the KV group are processed at
 //     once on the matrix cores:
 //       S^T[16 tok x 16]  = K_blk[16 x 128] . Q^T          4 x mfma 16x16x32 bf16
-//       V^T[16 dim x 16 tok] per 16 dims = V_blk . E_h      8 x mfma 16x16x32 bf16
-//         (E_h is a 0/1 selector; this transposes V exactly in registers)
-//       O^T[16 dim x 16]  += V^T . P^T                     8 x mfma 16x16x16 bf16,
-//         twice: P = P_hi + P_lo, both bf16, so P keeps ~16 mantissa bits.
+//       O^T[16 dim x 16]  += V^T . [P_hi; P_lo]^T          8 x mfma 16x16x32 bf16
+//         (one per 16 dimensions; the K index runs over the 16 tokens twice,
+//         against P_hi and P_lo, both bf16, so P keeps ~16 mantissa bits)
 //     K and V are read from HBM exactly once, with coalesced 16-byte loads
 //     (16 lanes per 256-byte token row), and pass through a wave-private,
-//     XOR-swizzled LDS tile into the MFMA operand layout.
+//     XOR-swizzled LDS tile: K is read back in the MFMA operand layout, V^T
+//     by the LDS transpose read, so every output dimension is computed from
+//     its own V column only.
 //   * A wave's issue priority falls by quarters of its token range, so that
 //     waves dispatched late are not starved by the older ones and the grid
 //     drains together.
@@ -172,11 +173,13 @@ __device__ __forceinline__ u32x4 buf_load16(__amdgpu_buffer_rsrc_t r, int voff, 
   return __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, kLoadAux));
 }
 
-// Process one 16-token block.  `valid` = tokens of the block inside the segment.
-__device__ __forceinline__ void attend_block(const u32x4 (&kr)[4], const u32x4 (&vr)[4],
-                                             const bf16x8 (&qb)[4], const bf16x8 (&sel)[2],
-                                             int valid, int c, float scale_log2, Softmax& st,
-                                             f32x4 (&o)[8]) {
+// Process one 16-token block.  `valid` = tokens of the block inside the segment;
+// lds_v points at this lane's transpose-read address in the block's V tile
+// (token 4c + n / 4, dimensions 4 (n % 4) .. 4 (n % 4) + 3 of dimension group 0),
+// v_step(nb) the element offset of dimension group nb from it.
+__device__ __forceinline__ void attend_block(const u32x4 (&kr)[4], const uint16_t* lds_v, const int (&v_off)[8],
+                                             const bf16x8 (&qb)[4], int valid, int c, float scale_log2,
+                                             Softmax& st, f32x4 (&o)[8]) {
   // logits: lane (c, n) gets tokens 4c+i, query n
   f32x4 s = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
@@ -195,9 +198,9 @@ __device__ __forceinline__ void attend_block(const u32x4 (&kr)[4], const u32x4 (
   if (__any(mx > st.m + kLazyRescale)) {
     const float m_new = fmaxf(st.m, mx);
     const float alpha = fast_exp2(st.m - m_new);  // 0 on the first block (m = -inf)
-    st.l *= alpha;
 #pragma unroll
     for (int nb = 0; nb < 8; ++nb) o[nb] *= alpha;
+    st.l *= alpha;
     st.m = m_new;
   }
   float p[4];
@@ -205,8 +208,9 @@ __device__ __forceinline__ void attend_block(const u32x4 (&kr)[4], const u32x4 (
   for (int i = 0; i < 4; ++i) p[i] = fast_exp2(x[i] - st.m);
   st.l += (p[0] + p[1]) + (p[2] + p[3]);
 
-  // P as the B operand of a 16x16x16 MFMA: slot (c, j) = token 4c + j.
-  // Split into hi + lo bf16 parts.
+  // P as the B operand of a 16x16x32 MFMA whose K index 8c + j is token 4c + j
+  // of P_hi (j < 4) and of P_lo (j >= 4): P = P_hi + P_lo keeps ~16 significant
+  // bits, and one product takes both terms.
   float hi[4], lo[4];
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
@@ -215,19 +219,15 @@ __device__ __forceinline__ void attend_block(const u32x4 (&kr)[4], const u32x4 (
   }
   const s16x4 p_hi = pack_bf16x4(hi[0], hi[1], hi[2], hi[3]);
   const s16x4 p_lo = pack_bf16x4(lo[0], lo[1], lo[2], lo[3]);
+  const bf16x8 pb = __builtin_bit_cast(bf16x8, __builtin_shufflevector(p_hi, p_lo, 0, 1, 2, 3, 4, 5, 6, 7));
 
-  const f32x4 zero = {0.f, 0.f, 0.f, 0.f};
+  // V^T straight from the LDS tile: the transpose read gives lane (c, n)
+  // V[token 4c + j][dimension 16 nb + n], j < 4, taken twice (against P_hi and P_lo)
 #pragma unroll
-  for (int kk = 0; kk < 4; ++kk) {
-#pragma unroll
-    for (int h = 0; h < 2; ++h) {
-      // lane (c, n): V[token 4c+i][dim 32kk + 16h + n], exact
-      const f32x4 t = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(vr[kk]), sel[h], zero, 0, 0, 0);
-      const s16x4 vt = pack_bf16x4(t[0], t[1], t[2], t[3]);
-      const int nb = 2 * kk + h;
-      o[nb] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(vt, p_hi, o[nb], 0, 0, 0);
-      o[nb] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(vt, p_lo, o[nb], 0, 0, 0);
-    }
+  for (int nb = 0; nb < 8; ++nb) {
+    const s16x4 vt = lds_read_tr16(lds_v + v_off[nb]);
+    const bf16x8 va = __builtin_bit_cast(bf16x8, __builtin_shufflevector(vt, vt, 0, 1, 2, 3, 0, 1, 2, 3));
+    o[nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(va, pb, o[nb], 0, 0, 0);
   }
 }
 
@@ -283,12 +283,17 @@ __global__ __launch_bounds__(64 * kWgWaves) __attribute__((amdgpu_waves_per_eu(k
   }
   const int64_t we = ws + width < total ? ws + width : total;
 
-  // selectors E_h: lane (c, n), slot j is 1 iff dim 8c + j == 16h + n
-  bf16x8 sel[2];
+  // LDS offsets of this lane's operand reads: K rows (token n, chunk 4kk + c)
+  // and the V transpose reads (token 4c + n / 4, dimensions 16 nb + 4 (n % 4) ..)
+  int k_off[4], v_off[8];
 #pragma unroll
-  for (int h = 0; h < 2; ++h)
+  for (int kk = 0; kk < 4; ++kk) k_off[kk] = n * kHeadDim + (((4 * kk + c) ^ tile_swizzle(n)) << 3);
+  {
+    const int v_tok = 4 * c + (n >> 2);
 #pragma unroll
-    for (int j = 0; j < 8; ++j) sel[h][j] = (8 * c + j == 16 * h + n) ? (__bf16)1.0f : (__bf16)0.0f;
+    for (int nb = 0; nb < 8; ++nb)
+      v_off[nb] = v_tok * kHeadDim + (((2 * nb + ((n & 3) >> 1)) ^ tile_swizzle(v_tok)) << 3) + 4 * (n & 1);
+  }
 
   const size_t row_elems = (size_t)p.hkv * kHeadDim;
   while (b < p.num_seqs && pos < we) {
@@ -393,7 +398,7 @@ __global__ __launch_bounds__(64 * kWgWaves) __attribute__((amdgpu_waves_per_eu(k
 #pragma unroll
         for (int u = 0; u < 4; ++u) {
           const int tok = 4 * u + ld_tok;
-          const int slot = tok * kHeadDim + (((lane & 15) ^ tok) << 3);
+          const int slot = tok * kHeadDim + (((lane & 15) ^ tile_swizzle(tok)) << 3);
           *reinterpret_cast<u32x4*>(&lds_k[slot]) = pk[u];
           *reinterpret_cast<u32x4*>(&lds_v[slot]) = pv[u];
         }
@@ -405,7 +410,7 @@ __global__ __launch_bounds__(64 * kWgWaves) __attribute__((amdgpu_waves_per_eu(k
             const size_t src = ((size_t)b * p.hkv + kv) * kHeadDim + 8 * lane;
             const u32x4 nk = load16(pg.k_new + src);
             const u32x4 nv = load16(pg.v_new + src);
-            const int slot = tok * kHeadDim + ((lane ^ tok) << 3);
+            const int slot = tok * kHeadDim + ((lane ^ tile_swizzle(tok)) << 3);
             *reinterpret_cast<u32x4*>(&lds_k[slot]) = nk;
             *reinterpret_cast<u32x4*>(&lds_v[slot]) = nv;
             const size_t dst = (blk_row + tok) * row_elems + (size_t)kv * kHeadDim + 8 * lane;
@@ -415,14 +420,10 @@ __global__ __launch_bounds__(64 * kWgWaves) __attribute__((amdgpu_waves_per_eu(k
         }
         const size_t next_row = issue(t + kBlock);
         __builtin_amdgcn_wave_barrier();
-        u32x4 kr[4], vr[4];
+        u32x4 kr[4];
 #pragma unroll
-        for (int kk = 0; kk < 4; ++kk) {
-          const int slot = n * kHeadDim + (((4 * kk + c) ^ n) << 3);
-          kr[kk] = *reinterpret_cast<const u32x4*>(&lds_k[slot]);
-          vr[kk] = *reinterpret_cast<const u32x4*>(&lds_v[slot]);
-        }
-        attend_block(kr, vr, qb, sel, valid, c, p.scale_log2, st, o);
+        for (int kk = 0; kk < 4; ++kk) kr[kk] = *reinterpret_cast<const u32x4*>(&lds_k[k_off[kk]]);
+        attend_block(kr, lds_v, v_off, qb, valid, c, p.scale_log2, st, o);
         blk_row = next_row;
       }
 

@@ -57,12 +57,6 @@ struct PrefillPlan {
   float scale_log2;
 };
 
-// LDS tile of K or V: token row t holds its 16 chunks of 8 dimensions with
-// chunk ch at slot ch ^ prefill_swizzle(t): conflict-free for the staging
-// writes, the K operand reads (16 tokens x one chunk) and the transpose reads
-// (4 tokens x 4 dimensions per 16 lanes).
-__device__ __forceinline__ int prefill_swizzle(int t) { return ((t & 7) << 1) | ((t >> 3) & 1); }
-
 // Workgroup barrier with no memory fence: the caller has already waited for
 // its own loads into LDS that the other waves will read, and a fence would
 // also wait for the loads of later blocks still in flight.  The memory clobber
@@ -188,7 +182,7 @@ __global__ __launch_bounds__(64 * kPrefillWaves) __attribute__((amdgpu_waves_per
 #pragma unroll
   for (int r = 0; r < kPrefillLoads; ++r) {
     const int t = (tid >> 4) + r * 4 * kPrefillWaves;
-    dvo[r] = t * row_bytes + (((tid & 15) ^ prefill_swizzle(t)) << 4);
+    dvo[r] = t * row_bytes + (((tid & 15) ^ tile_swizzle(t)) << 4);
   }
   auto issue = [&](int tb, uint16_t* dk, uint16_t* dv) {
     // a block past kv_end gets an empty range: no memory access, zeros in LDS
@@ -209,10 +203,10 @@ __global__ __launch_bounds__(64 * kPrefillWaves) __attribute__((amdgpu_waves_per
   // per-lane LDS offsets of the operand reads within a 16-token half block
   int k_off[4];
 #pragma unroll
-  for (int kk = 0; kk < 4; ++kk) k_off[kk] = n * kHeadDim + (((4 * kk + c) ^ prefill_swizzle(n)) << 3);
+  for (int kk = 0; kk < 4; ++kk) k_off[kk] = n * kHeadDim + (((4 * kk + c) ^ tile_swizzle(n)) << 3);
   const int v_tok = 4 * c + (n >> 2);
   const int v_row = v_tok * kHeadDim + 4 * (n & 1);
-  const int v_swz = prefill_swizzle(v_tok);
+  const int v_swz = tile_swizzle(v_tok);
   const int v_ch = (n & 3) >> 1;
 
   // One 32-token block: wait for this wave's loads of it, then the barrier

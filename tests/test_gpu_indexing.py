@@ -303,3 +303,28 @@ def test_graph_capture_replay_matches_eager():
         torch.cuda.synchronize()
     del g
     attn.close()
+
+
+@pytest.mark.parametrize("split", [0, 16])
+def test_non_finite_value_reaches_only_its_own_dimension(split):
+    """out[b, h, d] depends on V[:, kv, d] only (eq:token-context, the
+    attention definition): a NaN or an infinity in one element of V makes that
+    output dimension of the heads reading it non-finite and leaves every other
+    element equal to the oracle's."""
+    rng = np.random.default_rng(61)
+    w = wl.Workload("nonfinite", 121, 1, 4, 32, 8, 1, "uniform", 40, 300)
+    lay = wl.workload_layout(w)
+    k, v = wl.layer_kv_bits(w, lay, 0)
+    q = wl.query_bits(w, 0)
+    planted = [(1, 7, 2, 37, wl.BF16_NAN), (2, 3, 5, 100, np.uint16(0x7F80)), (3, 0, 0, 5, np.uint16(0xFF80))]
+    for b, t, kv, d, bits in planted:
+        v[lay.offsets[b] + t, kv, d] = bits
+    ref = oracle.decode_attn(q, k, v, lay.offsets, lay.lens, w.scale)
+    got = run(32, 8, q, k, v, lay.offsets, lay.lens, w.scale, split_tokens=split)
+    bad = np.zeros(got.shape, bool)
+    g = w.group
+    for b, t, kv, d, _ in planted:
+        bad[b, kv * g:(kv + 1) * g, d] = True
+    assert not np.isfinite(got[bad]).any(), "a planted non-finite value did not reach its dimension"
+    assert np.isnan(got[1, 2 * g:3 * g, 37]).all()
+    assert_parity(got[~bad], ref[~bad], f"elements beside the non-finite ones, split={split}")
