@@ -200,3 +200,75 @@ def test_prefill_sequences_without_new_tokens():
         rows[qs[b]:qs[b] + nq[b]] = True
     assert_parity(got[rows], ref[rows], "with empty sequences", tight=False)
     assert (got[~rows] == -555.0).all(), "rows of sequences without new tokens were written"
+
+
+U_BF16 = 2.0 ** -9  # relative rounding error of round-to-nearest-even to bf16 (8 significant bits)
+
+
+def weighted_deviation(q_heads, h, hk, hv, off, length, scale, kv, ref_row):
+    """sum_t w_t |V[t, kv, :] - ref| for query head h of one row (q_heads
+    [Hq, D]): the oracle's weights (oracle.attn_weights) against the oracle's
+    output row."""
+    w = oracle.attn_weights(q_heads[None], hk, np.array([off], np.int32), np.array([length], np.int32), scale, 0, h)
+    vv = wl.bf16_bits_to_f32(hv[off:off + length, kv]).astype(np.float64)
+    return w @ np.abs(vv - ref_row[None, :])
+
+
+@pytest.mark.parametrize("hq", [32, 128], ids=["group4", "group16"])
+def test_prefill_bf16_weights_worst_case_against_the_rounding_bound(hq):
+    """The default precision (softmax weights rounded to bf16, rows normalised
+    by the sum of the rounded weights) at its worst case: 12k-token
+    histories, 5% of key rows x4 (peaky softmax), group sizes 4 and 16.
+
+    Bound: with p~_t = p_t (1 + d_t), |d_t| <= u = 2^-9, and weights
+    normalised by sum p~, the output error is
+        sum_t w_t (d_t - dbar) (V_t - out) / (1 + dbar),   dbar = sum_t w_t d_t,
+    (the d's enter only through their deviation from their weighted mean, so
+    any constant can be subtracted from V), hence
+        |err_d| <= 2u / (1 - u) * sum_t w_t |V_t,d - out_d|.
+    Every checked element must stay under it (plus 1e-4 for the fp32 logits
+    and accumulation); the margin against the 1e-2 gate is reported."""
+    rng = np.random.default_rng(200 + hq)
+    batch, hkv = 8, 8
+    nq = rng.integers(64, 257, size=batch).astype(np.int32)
+    lens = (rng.integers(11000, 12289, size=batch) + nq).astype(np.int32)
+    w = wl.Workload(f"pf_worst{hq}", 195 + hq % 7, 1, batch, hq, hkv, 1, "uniform", 1, 2, peaky_frac=0.05)
+    lay = wl.make_layout(lens, 1)
+    k = torch.empty((lay.num_rows, hkv, 128), dtype=torch.bfloat16, device=dev())
+    v = torch.empty_like(k)
+    wl.fill_kv_device(k, v, w, 0)
+    q_starts = np.concatenate([[0], np.cumsum(nq)[:-1]]).astype(np.int32)
+    q = torch.empty((int(nq.sum()), hq, 128), dtype=torch.bfloat16, device=dev())
+    wl.fill_normal_bf16_device(q, wl.DEFAULT_SEED, w.index, 0, 14)
+    out = torch.empty((int(nq.sum()), hq, 128), dtype=torch.float32, device=dev())
+    with DecodeAttention(hq, hkv, batch, int(lens.max())) as attn:
+        attn.prefill(q, k, v, up_i32(lay.offsets), up_i32(lens), up_i32(q_starts), up_i32(nq), int(nq.max()),
+                     w.scale, out)
+        torch.cuda.synchronize()
+    as_bits = lambda t: t.view(torch.int16).cpu().numpy().view(np.uint16)  # noqa: E731
+    hk, hv = as_bits(k), as_bits(v)
+    rows, offs, plen = [], [], []
+    for b in range(batch):
+        for i in sorted({0, int(nq[b]) - 1, *(int(x) for x in rng.integers(1, nq[b] - 1, size=2))}):
+            rows.append(int(q_starts[b]) + i)
+            offs.append(int(lay.offsets[b]))
+            plen.append(int(lens[b]) - int(nq[b]) + i + 1)
+    sel = torch.tensor(rows, device=dev())
+    qh = as_bits(q[sel])
+    got = out[sel].cpu().numpy().astype(np.float64)
+    ref = oracle.decode_attn(qh, hk, hv, np.array(offs, np.int32), np.array(plen, np.int32), w.scale)
+    from concurrent.futures import ThreadPoolExecutor
+
+    g = hq // hkv
+    jobs = [(r, h) for r in range(len(rows)) for h in range(hq)]
+    with ThreadPoolExecutor(max_workers=16) as pool:
+        devs = list(pool.map(lambda rh: weighted_deviation(qh[rh[0]], rh[1], hk, hv, offs[rh[0]], plen[rh[0]],
+                                                          w.scale, rh[1] // g, ref[rh[0], rh[1]]), jobs))
+    dev_arr = np.stack(devs).reshape(len(rows), hq, 128)
+    bound = 2 * U_BF16 / (1 - U_BF16) * dev_arr + 1e-4
+    err = np.abs(got - ref)
+    mx = float(err.max())
+    print(f"group {g}: {len(rows)} rows x {hq} heads, max-abs {mx:.3e} (margin {1e-2 - mx:.3e} to the 1e-2 gate), "
+          f"largest err / bound {float((err / bound).max()):.3f}, largest bound {float(bound.max()):.3e}", flush=True)
+    assert (err <= bound).all(), f"error above the bf16-weight rounding bound at {np.argwhere(err > bound)[:5]}"
+    assert_parity(got, ref, f"prefill worst case, group {g}", tight=False)
