@@ -163,6 +163,20 @@ def copy_ceiling(torch, dev, achieved_gbs: float) -> dict:
                       f"median of {r['reps']} in this process"}
 
 
+def mfma_ceiling(torch, dev, achieved_tflops: float) -> dict:
+    """The bf16 matrix-core rate the prefill kernel's instruction shape
+    (v_mfma_f32_16x16x32_bf16) sustains on this device (ctx_mfma_bf16, 2 waves
+    per SIMD as the prefill kernel runs, median of 5 launches) in this process,
+    and the fraction of it that `achieved_tflops` reaches."""
+    from paper_2609_36608_amd import binding
+    from paper_2609_36608_amd import rollout_calibration as rcal
+
+    r = rcal.measure_mfma(torch, dev, binding.CTX_MFMA_16X16X32, waves_per_simd=2)
+    return {"mfma_tflops": r["tflops"], "best_tflops": r["best_tflops"], "frac": round(achieved_tflops / r["tflops"], 4),
+            "source": "ctx_mfma_bf16 (8 chains of v_mfma_f32_16x16x32_bf16 per wave, 2 waves per SIMD), "
+                      "median of 5 in this process"}
+
+
 CEILING_METRIC = "HBM streaming ceiling GB/s (fraction of 8 TB/s peak), 1 MI355X"
 
 
@@ -171,6 +185,7 @@ def bench_ceiling(args) -> int:
     (ctx_hbm_read, ctx_hbm_copy) over 8 GiB, each launched --steps times."""
     import torch
 
+    from paper_2609_36608_amd import binding
     from paper_2609_36608_amd import rollout_calibration as rcal
 
     if not torch.cuda.is_available():
@@ -182,6 +197,10 @@ def bench_ceiling(args) -> int:
     for name, copy, nt in (("read_nt", False, True), ("read_cached", False, False), ("copy_nt", True, True),
                            ("copy_cached", True, False)):
         res[name] = rcal.measure_hbm(torch, dev, gib=8.0, reps=args.steps, copy=copy, nontemporal=nt)
+    mfma = {}
+    for shape, name in ((binding.CTX_MFMA_16X16X32, "mfma_16x16x32"), (binding.CTX_MFMA_32X32X16, "mfma_32x32x16")):
+        for wps in (1, 2):
+            mfma[f"{name}_{wps}w"] = rcal.measure_mfma(torch, dev, shape, waves_per_simd=wps, reps=args.steps)
     best = res["read_nt"]
     result = {
         "metric": CEILING_METRIC,
@@ -201,6 +220,7 @@ def bench_ceiling(args) -> int:
         "frac_of_hbm_peak": round(best["gbs"] / HBM_PEAK_GBS, 4),
         "kernels": {k: {kk: v[kk] for kk in ("gbs", "best_gbs", "workgroups", "nontemporal", "kernel")}
                     for k, v in res.items()},
+        "matrix_cores": {**mfma, "peak_tflops": MFMA_BF16_PEAK_TFLOPS},
         "device": device_info(torch, dev),
     }
     print(json.dumps(result), flush=True)
@@ -368,6 +388,7 @@ def bench_prefill(args) -> int:
             "peak": MFMA_BF16_PEAK_TFLOPS,
             "unit": "TFLOP/s",
             "frac": round(flops / (elapsed_s / calls) / 1e12 / MFMA_BF16_PEAK_TFLOPS, 4),
+            "ceiling": mfma_ceiling(torch, dev, flops / (elapsed_s / calls) / 1e12),
             **traffic_fields(w.name, "prefill_kernel"),
             "kernel": ("prefill_kernel (one ctx_prefill_attn_run call per layer, "
                        + ("two-term softmax weights)" if args.prefill_p == "split" else "bf16 softmax weights)")),

@@ -1,6 +1,6 @@
 /*
- * ctx_hbm_probe.h -- streaming kernels that measure the practical HBM ceiling
- * of the device the library runs on.
+ * ctx_ceiling_probe.h -- kernels that measure the practical ceilings of the
+ * device the library runs on: HBM streaming and the bf16 matrix-core rate.
  *
  * The decode step is bound by reading the KV cache (and, per step, the
  * student's weights) from HBM once.  The rollout engine model of the
@@ -15,8 +15,8 @@
  * `stream` is a hipStream_t passed as void* (NULL = default stream); the calls
  * are asynchronous (no host sync, no allocation) and return ctx_status codes.
  */
-#ifndef CTX_HBM_PROBE_H_
-#define CTX_HBM_PROBE_H_
+#ifndef CTX_CEILING_PROBE_H_
+#define CTX_CEILING_PROBE_H_
 
 #include <stddef.h>
 #include <stdint.h>
@@ -49,8 +49,27 @@ int ctx_hbm_read(const void* src, size_t bytes, void* sink, int32_t workgroups, 
  */
 int ctx_hbm_copy(const void* src, void* dst, size_t bytes, int32_t workgroups, uint32_t flags, void* stream);
 
+/*
+ * Matrix-core rate: every wave of `workgroups` workgroups of 256 threads runs
+ * `iterations` rounds of 8 independent bf16 MFMAs with fp32 accumulation and
+ * writes one 16-byte word per wave to sink, like ctx_hbm_read.  The causal
+ * prefill of the reference observation (Sec. 4.1,
+ * eq:reference-conditioned-action) is a dense contraction on these units;
+ * this gives the rate they sustain on this device for its instruction shapes.
+ *   shape       CTX_MFMA_16X16X32 (8 x v_mfma_f32_16x16x32_bf16 per round: 131,072
+ *               flops per wave) or CTX_MFMA_32X32X16 (8 x v_mfma_f32_32x32x16_bf16:
+ *               262,144 flops per wave)
+ *   workgroups  1 .. 65536; iterations 1 .. 1<<20
+ *   sink        16-byte aligned, workgroups * CTX_HBM_SINK_BYTES_PER_WORKGROUP bytes
+ * Flops per call = workgroups * 4 * iterations * (flops per wave per round).
+ * Errors: INVALID_ARG (shape, sizes, NULL), ALIGNMENT, HIP.
+ */
+#define CTX_MFMA_16X16X32 0
+#define CTX_MFMA_32X32X16 1
+int ctx_mfma_bf16(int32_t shape, int32_t workgroups, int32_t iterations, void* sink, void* stream);
+
 #ifdef __cplusplus
 }
 #endif
 
-#endif /* CTX_HBM_PROBE_H_ */
+#endif /* CTX_CEILING_PROBE_H_ */

@@ -199,7 +199,7 @@ int ctx_decode_attn_run_paged(ctx_decode_attn* handle, const void* q, void* k_pa
  *   flags        0 or CTX_PREFILL_SPLIT_P.  With 0 the softmax weights enter the
  *                P.V product rounded to bf16 (nearest even), and each row is
  *                normalised by the sum of the rounded weights, so it stays a convex
- *                combination of V rows (weights within 2^-9 relative of exact; a few
+ *                combination of V rows (weights within 2^-8 relative of exact; a few
  *                1e-3 absolute on N(0,1) data).  CTX_PREFILL_SPLIT_P carries the
  *                weights as two bf16 terms (16 significant bits; about 1e-6
  *                absolute) at half again the matrix-core work.

@@ -26,6 +26,9 @@ CTX_PREFILL_SPLIT_P = 1  # ctx_prefill_attn_run flag: softmax weights as two bf1
 CTX_STATIC_SCRATCH_BYTES = 16 << 20  # static workspace of ctx_decode_attn_run_static, per device
 CTX_HBM_SINK_BYTES_PER_WORKGROUP = 64
 CTX_HBM_NONTEMPORAL = 1
+CTX_MFMA_16X16X32 = 0
+CTX_MFMA_32X32X16 = 1
+MFMA_FLOPS_PER_WAVE_ROUND = {CTX_MFMA_16X16X32: 8 * 16 * 16 * 32 * 2, CTX_MFMA_32X32X16: 8 * 32 * 32 * 16 * 2}
 
 # every function the C header declares
 EXPORTS = (
@@ -39,6 +42,7 @@ EXPORTS = (
     "ctx_rollout_simulate_engine",
     "ctx_hbm_read",
     "ctx_hbm_copy",
+    "ctx_mfma_bf16",
     "ctx_decode_attn_destroy",
     "ctx_decode_attn_status_string",
     "ctx_decode_attn_last_error",
@@ -133,6 +137,8 @@ def load_library(path: str | None = None):
     lib.ctx_hbm_read.restype = ctypes.c_int
     lib.ctx_hbm_copy.argtypes = [vp, vp, ctypes.c_size_t, i32, ctypes.c_uint32, vp]
     lib.ctx_hbm_copy.restype = ctypes.c_int
+    lib.ctx_mfma_bf16.argtypes = [i32, i32, i32, vp, vp]
+    lib.ctx_mfma_bf16.restype = ctypes.c_int
     lib.ctx_decode_attn_destroy.argtypes = [vp]
     lib.ctx_decode_attn_destroy.restype = ctypes.c_int
     lib.ctx_decode_attn_status_string.argtypes = [ctypes.c_int]
@@ -478,3 +484,15 @@ def ctx_hbm_copy(src, dst, workgroups: int, nontemporal: bool = True, stream=Non
                           CTX_HBM_NONTEMPORAL if nontemporal else 0, _stream_ptr(stream, src.device))
     if rc != CTX_OK:
         raise error_for(lib, rc)
+
+
+def ctx_mfma_bf16(shape: int, workgroups: int, iterations: int, sink, stream=None) -> int:
+    """Run the matrix-core rate probe (ctx_mfma_bf16); returns the flops it performs.
+    `sink` is a CUDA tensor of at least workgroups * 64 bytes."""
+    lib = load_library()
+    if sink.numel() * sink.element_size() < workgroups * CTX_HBM_SINK_BYTES_PER_WORKGROUP:
+        raise ValueError("sink must hold workgroups * 64 bytes")
+    rc = lib.ctx_mfma_bf16(int(shape), int(workgroups), int(iterations), sink.data_ptr(), _stream_ptr(stream, sink.device))
+    if rc != CTX_OK:
+        raise error_for(lib, rc)
+    return workgroups * 4 * iterations * MFMA_FLOPS_PER_WAVE_ROUND[shape]

@@ -12,7 +12,7 @@ PKG = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(PKG)
 SRC = os.path.join(PKG, "csrc", "ctx_decode_attn.hip")
 SRCS = [SRC, os.path.join(PKG, "csrc", "ctx_prefill_attn.hip"), os.path.join(PKG, "csrc", "ctx_opd_loss.hip"),
-        os.path.join(PKG, "csrc", "ctx_hbm_probe.hip"), os.path.join(PKG, "csrc", "ctx_rollout_sim.cpp")]
+        os.path.join(PKG, "csrc", "ctx_ceiling_probe.hip"), os.path.join(PKG, "csrc", "ctx_rollout_sim.cpp")]
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "libctx_decode_attn.so")
 ARCH = "gfx950"

@@ -1,6 +1,6 @@
-// ctx_hbm_probe.hip -- streaming read and copy kernels for gfx950 (MI355X)
-// that measure the device's practical HBM ceiling, behind the C ABI declared
-// in include/ctx_hbm_probe.h.
+// ctx_ceiling_probe.hip -- kernels for gfx950 (MI355X) that measure the
+// device's practical ceilings (streaming read and copy; the bf16 matrix-core
+// rate), behind the C ABI declared in include/ctx_ceiling_probe.h.
 //
 // Both kernels run a grid-stride loop over tiles of kProbeThreads x
 // kProbeUnroll 16-byte words: every thread issues kProbeUnroll independent
@@ -15,7 +15,7 @@
 #include <cstdint>
 
 #include "ctx_attn_common.h"
-#include "ctx_hbm_probe.h"
+#include "ctx_ceiling_probe.h"
 
 namespace {
 
@@ -82,6 +82,48 @@ __global__ __launch_bounds__(kProbeThreads) void hbm_copy_kernel(const u32x4* __
   }
 }
 
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+constexpr int kMfmaChains = 8;
+
+// 8 independent accumulation chains per wave, operands that vary per lane;
+// the results are folded into one word per wave so that no MFMA is dead.
+template <int kShape>
+__global__ __launch_bounds__(kProbeThreads) void mfma_probe_kernel(int iterations, u32x4* __restrict__ sink) {
+  bf16x8 a, b;
+#pragma unroll
+  for (int j = 0; j < 8; ++j) {
+    a[j] = (__bf16)((float)((threadIdx.x + j) & 7) * 0.125f);
+    b[j] = (__bf16)((float)((threadIdx.x * 3 + j) & 7) * 0.0625f);
+  }
+  float fold = 0.f;
+  if (kShape == CTX_MFMA_16X16X32) {
+    f32x4 acc[kMfmaChains];
+#pragma unroll
+    for (int k = 0; k < kMfmaChains; ++k) acc[k] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int it = 0; it < iterations; ++it) {
+#pragma unroll
+      for (int k = 0; k < kMfmaChains; ++k) acc[k] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, acc[k], 0, 0, 0);
+    }
+#pragma unroll
+    for (int k = 0; k < kMfmaChains; ++k) fold += acc[k][0] + acc[k][3];
+  } else {
+    f32x16 acc[kMfmaChains];
+#pragma unroll
+    for (int k = 0; k < kMfmaChains; ++k) acc[k] = f32x16{};
+    for (int it = 0; it < iterations; ++it) {
+#pragma unroll
+      for (int k = 0; k < kMfmaChains; ++k) acc[k] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, acc[k], 0, 0, 0);
+    }
+#pragma unroll
+    for (int k = 0; k < kMfmaChains; ++k) fold += acc[k][0] + acc[k][15];
+  }
+  u32x4 w = {__float_as_uint(fold), 0u, 0u, 0u};
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) w.x ^= __shfl_xor(w.x, off);
+  if ((threadIdx.x & 63) == 0) sink[(size_t)blockIdx.x * (kProbeThreads / 64) + (threadIdx.x >> 6)] = w;
+}
+
 int check_probe(const void* src, const void* other, size_t bytes, int32_t workgroups, uint32_t flags) {
   ctx_clear_error();
   if (src == nullptr || other == nullptr) return fail(CTX_ERR_INVALID_ARG, "NULL pointer");
@@ -122,6 +164,25 @@ extern "C" int ctx_hbm_copy(const void* src, void* dst, size_t bytes, int32_t wo
     hipLaunchKernelGGL(hbm_copy_kernel<true>, dim3(workgroups), dim3(kProbeThreads), 0, s, sp, dp, bytes / 16);
   else
     hipLaunchKernelGGL(hbm_copy_kernel<false>, dim3(workgroups), dim3(kProbeThreads), 0, s, sp, dp, bytes / 16);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return hip_fail(e, "kernel launch");
+  return CTX_OK;
+}
+
+extern "C" int ctx_mfma_bf16(int32_t shape, int32_t workgroups, int32_t iterations, void* sink, void* stream) {
+  ctx_clear_error();
+  if (sink == nullptr) return fail(CTX_ERR_INVALID_ARG, "NULL sink");
+  if (shape != CTX_MFMA_16X16X32 && shape != CTX_MFMA_32X32X16) return fail(CTX_ERR_INVALID_ARG, "unknown shape %d", shape);
+  if (workgroups < 1 || workgroups > kProbeMaxGrid)
+    return fail(CTX_ERR_INVALID_ARG, "workgroups %d outside 1..%d", workgroups, kProbeMaxGrid);
+  if (iterations < 1 || iterations > (1 << 20)) return fail(CTX_ERR_INVALID_ARG, "iterations %d outside 1..2^20", iterations);
+  if (!aligned16(sink)) return fail(CTX_ERR_ALIGNMENT, "sink must be 16-byte aligned");
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  u32x4* kp = static_cast<u32x4*>(sink);
+  if (shape == CTX_MFMA_16X16X32)
+    hipLaunchKernelGGL(mfma_probe_kernel<CTX_MFMA_16X16X32>, dim3(workgroups), dim3(kProbeThreads), 0, s, iterations, kp);
+  else
+    hipLaunchKernelGGL(mfma_probe_kernel<CTX_MFMA_32X32X16>, dim3(workgroups), dim3(kProbeThreads), 0, s, iterations, kp);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return hip_fail(e, "kernel launch");
   return CTX_OK;

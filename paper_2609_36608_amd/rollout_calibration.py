@@ -84,6 +84,31 @@ def measure_hbm(torch, dev, gib: float = 4.0, reps: int = 8, copy: bool = False,
             "kernel": "ctx_hbm_copy" if copy else "ctx_hbm_read"}
 
 
+def measure_mfma(torch, dev, shape: int = binding.CTX_MFMA_16X16X32, waves_per_simd: int = 2,
+                 iterations: int = 4096, reps: int = 5) -> dict:
+    """bf16 matrix-core rate of ctx_mfma_bf16 (TFLOP/s, median and best of
+    `reps` timed launches after one untimed one), with `waves_per_simd`
+    four-wave workgroups per compute unit."""
+    cus = torch.cuda.get_device_properties(dev).multi_processor_count
+    workgroups = cus * waves_per_simd
+    sink = torch.empty(workgroups * binding.CTX_HBM_SINK_BYTES_PER_WORKGROUP, dtype=torch.uint8, device=dev)
+    stream = torch.cuda.current_stream(dev)
+    binding.ctx_mfma_bf16(shape, workgroups, iterations, sink, stream)
+    torch.cuda.synchronize(dev)
+    rates = []
+    for _ in range(reps):
+        e0, e1 = _events(torch)
+        e0.record(stream)
+        flops = binding.ctx_mfma_bf16(shape, workgroups, iterations, sink, stream)
+        e1.record(stream)
+        e1.synchronize()
+        rates.append(flops / (e0.elapsed_time(e1) / 1e3) / 1e12)
+    rates.sort()
+    return {"tflops": round(float(np.median(rates)), 1), "best_tflops": round(rates[-1], 1),
+            "shape": "16x16x32" if shape == binding.CTX_MFMA_16X16X32 else "32x32x16",
+            "waves_per_simd": waves_per_simd, "kernel": "ctx_mfma_bf16"}
+
+
 def calibrate_attention(torch, dev, points=POINTS_FULL, reps: int = 40) -> dict:
     """Seconds per ctx_decode_attn_run call at the student's shape for each
     (batch, context) point, every point cycling distinct K/V caches of at

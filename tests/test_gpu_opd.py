@@ -16,8 +16,9 @@ pytestmark = pytest.mark.gpu
 
 # Tolerances from the arithmetic: the fp32 log-sum-exp over <= 155k terms is
 # good to a few 1e-6 absolute, so lp, the ratio and the token losses carry
-# relative errors near 1e-6; gradients are rounded to bf16 (half an ulp is
-# 2^-9 relative), checked at 2^-8 relative plus 1e-5 of the row's scale.
+# relative errors near 1e-6; gradients are rounded to bf16 (half an ulp is at
+# most 2^-8 relative: 8 significant bits), checked at 2^-8 relative plus 1e-5
+# of the row's scale.
 LP_ATOL = 1e-4
 LOSS_RTOL, LOSS_ATOL = 1e-4, 1e-5
 GRAD_RTOL = 2.0 ** -8

@@ -92,7 +92,7 @@ def test_prefill_constant_v(split_p):
     """V rows all equal: every output row is that row, to fp32 rounding, in both
     modes.  In the default mode this holds only because each row is normalised
     by the sum of the rounded weights that the P.V product uses (normalising by
-    the unrounded sum would be off by up to 2^-9 relative)."""
+    the unrounded sum would be off by up to 2^-8 relative)."""
     w, lay, lens, nq, qs, q, k, v = prefill_case(23, 32, 8, batch=5, hist=(0, 700), new=(1, 200), peaky=True)
     row = wl.f32_to_bf16_bits(np.random.default_rng(5).standard_normal((8, 128)).astype(np.float32) * 3)
     used = np.zeros(v.shape[0], bool)
@@ -108,7 +108,7 @@ def test_prefill_constant_v(split_p):
     print(f"constant V split_p={split_p}: max-abs {err:.3e}, max |V| {cmax:.2f}", flush=True)
     # two terms carry each weight to within 2^-17 relative; one bf16 term with
     # the matching normaliser is exact up to fp32 accumulation.  Normalising
-    # the bf16 weights by the unrounded sum would be off by up to 2^-9 |V|.
+    # the bf16 weights by the unrounded sum would be off by up to 2^-8 |V|.
     assert err <= (2.0**-14 if split_p else 2.0**-16) * cmax
 
 
@@ -202,7 +202,7 @@ def test_prefill_sequences_without_new_tokens():
     assert (got[~rows] == -555.0).all(), "rows of sequences without new tokens were written"
 
 
-U_BF16 = 2.0 ** -9  # relative rounding error of round-to-nearest-even to bf16 (8 significant bits)
+U_BF16 = 2.0 ** -8  # unit roundoff of round-to-nearest-even to bf16 (8 significant bits)
 
 
 def weighted_deviation(q_heads, h, hk, hv, off, length, scale, kv, ref_row):
@@ -220,7 +220,7 @@ def test_prefill_bf16_weights_worst_case_against_the_rounding_bound(hq):
     by the sum of the rounded weights) at its worst case: 12k-token
     histories, 5% of key rows x4 (peaky softmax), group sizes 4 and 16.
 
-    Bound: with p~_t = p_t (1 + d_t), |d_t| <= u = 2^-9, and weights
+    Bound: with p~_t = p_t (1 + d_t), |d_t| <= u = 2^-8, and weights
     normalised by sum p~, the output error is
         sum_t w_t (d_t - dbar) (V_t - out) / (1 + dbar),   dbar = sum_t w_t d_t,
     (the d's enter only through their deviation from their weighted mean, so
