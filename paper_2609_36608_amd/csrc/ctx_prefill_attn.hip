@@ -77,7 +77,8 @@ __device__ __forceinline__ void split_bf16x2(float a, float b, uint32_t* hi, uin
 // gives a NaN weight either way.
 __device__ __forceinline__ float max8(float a, float b, float c, float d, float e, float f, float g, float h) {
   const auto mx = [](float x, float y) { return __builtin_elementwise_maximum(x, y); };
-  return mx(mx(mx(a, b), mx(c, d)), mx(mx(e, f), mx(g, h)));
+  // grouped so that the three-input form covers it in 4 instructions
+  return mx(mx(mx(mx(a, b), c), mx(mx(d, e), f)), mx(g, h));
 }
 
 template <typename OutT, bool kSplitP>
@@ -311,12 +312,21 @@ __global__ __launch_bounds__(64 * kPrefillWaves) __attribute__((amdgpu_waves_per
       // The MFMA stream runs at raised wave priority, so that the other wave
       // on this SIMD fills the matrix core's issue gaps with its softmax.
       __builtin_amdgcn_s_setprio(1);
+      // The V^T reads of dimension group nb + 1 are issued before the
+      // products of group nb (the scheduling barrier keeps the compiler from
+      // sinking them to their use), so their latency hides behind those.
+      auto read_vt = [&](int nb, s16x4& v0, s16x4& v1) {
+        const int off = v_row + (((2 * nb + v_ch) ^ v_swz) << 3);
+        v0 = lds_read_tr16(vt + off);
+        v1 = lds_read_tr16(vt + 16 * kHeadDim + off);
+      };
+      s16x4 nv0, nv1;
+      read_vt(0, nv0, nv1);
 #pragma unroll
       for (int nb = 0; nb < 8; ++nb) {
-        const int off = v_row + (((2 * nb + v_ch) ^ v_swz) << 3);
-        const s16x4 v0 = lds_read_tr16(vt + off);
-        const s16x4 v1 = lds_read_tr16(vt + 16 * kHeadDim + off);
-        const bf16x8 va = __builtin_bit_cast(bf16x8, __builtin_shufflevector(v0, v1, 0, 1, 2, 3, 4, 5, 6, 7));
+        const bf16x8 va = __builtin_bit_cast(bf16x8, __builtin_shufflevector(nv0, nv1, 0, 1, 2, 3, 4, 5, 6, 7));
+        if (nb + 1 < 8) read_vt(nb + 1, nv0, nv1);
+        __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
         for (int ct = 0; ct < kPrefillTiles; ++ct)
           o[ct][nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(va, as_bf16x8(phi[ct]), o[ct][nb], 0, 0, 0);
