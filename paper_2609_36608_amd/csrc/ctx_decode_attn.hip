@@ -557,24 +557,38 @@ int split_waves(int hkv) {
   return wgw;
 }
 
-// Ranges of the balanced split for the contiguous ([0]) and paged ([1])
-// kernels: enough that one wave per (range, KV head) is resident at once, in
-// whole multiples of the XCD count.
-int balanced_ranges(const ctx_decode_attn_desc& d, int cus, int wgw, int64_t ranges[2]) {
+// Resident waves per CU of the split kernel for the contiguous ([0]) and
+// paged ([1]) layouts with wgw-wave workgroups; they depend on the output
+// dtype and wgw only.
+int resident_waves(int32_t out_dtype, int wgw, int64_t per_cu[2]) {
   const void* kernels[2] = {
-      d.out_dtype == CTX_DTYPE_F32 ? reinterpret_cast<const void*>(&decode_split_kernel<float, false>)
-                                   : reinterpret_cast<const void*>(&decode_split_kernel<uint16_t, false>),
-      d.out_dtype == CTX_DTYPE_F32 ? reinterpret_cast<const void*>(&decode_split_kernel<float, true>)
-                                   : reinterpret_cast<const void*>(&decode_split_kernel<uint16_t, true>)};
+      out_dtype == CTX_DTYPE_F32 ? reinterpret_cast<const void*>(&decode_split_kernel<float, false>)
+                                 : reinterpret_cast<const void*>(&decode_split_kernel<uint16_t, false>),
+      out_dtype == CTX_DTYPE_F32 ? reinterpret_cast<const void*>(&decode_split_kernel<float, true>)
+                                 : reinterpret_cast<const void*>(&decode_split_kernel<uint16_t, true>)};
   for (int layout = 0; layout < 2; ++layout) {
     int n = 0;
     hipError_t e =
         hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, kernels[layout], 64 * wgw, (size_t)wgw * kTileBytes);
     if (e != hipSuccess) return hip_fail(e, "hipOccupancyMaxActiveBlocksPerMultiprocessor");
-    const int64_t per_cu = n < 1 ? 1 : (int64_t)n * wgw;  // resident waves per CU
-    ranges[layout] = (int64_t)cus * per_cu / d.num_kv_heads / kXcds * kXcds;
-    if (ranges[layout] < kXcds) ranges[layout] = kXcds;
+    per_cu[layout] = n < 1 ? 1 : (int64_t)n * wgw;
   }
+  return CTX_OK;
+}
+
+// Ranges of the balanced split: enough that one wave per (range, KV head) is
+// resident at once, in whole multiples of the XCD count.
+int64_t ranges_for(int cus, int64_t per_cu, int hkv) {
+  const int64_t r = (int64_t)cus * per_cu / hkv / kXcds * kXcds;
+  return r < kXcds ? kXcds : r;
+}
+
+// Ranges of the balanced split for the contiguous ([0]) and paged ([1]) kernels.
+int balanced_ranges(const ctx_decode_attn_desc& d, int cus, int wgw, int64_t ranges[2]) {
+  int64_t per_cu[2];
+  const int rc = resident_waves(d.out_dtype, wgw, per_cu);
+  if (rc != CTX_OK) return rc;
+  for (int layout = 0; layout < 2; ++layout) ranges[layout] = ranges_for(cus, per_cu[layout], d.num_kv_heads);
   return CTX_OK;
 }
 
@@ -824,7 +838,7 @@ struct StaticDevice {
   bool ready;
   int cus;
   unsigned char* scratch;     // device address of `scratch` on this device
-  int32_t ranges[2][kWgWaves + 1];  // balanced ranges per out dtype and waves per workgroup (0: not yet known)
+  int64_t per_cu[2][kWgWaves + 1];  // resident split waves per CU by out dtype and waves per workgroup (0: not yet known)
 };
 
 StaticDevice g_static[kMaxDevices];
@@ -882,17 +896,19 @@ extern "C" int ctx_decode_attn_run_static(const ctx_decode_attn_desc* desc, cons
     rc = static_device(dev, &sd);
     if (rc != CTX_OK) return rc;
     const int wgw = split_waves(d.num_kv_heads);
-    int32_t& ranges = sd->ranges[d.out_dtype == CTX_DTYPE_F32 ? 1 : 0][wgw];
-    if (ranges == 0) {
+    int64_t& per_cu = sd->per_cu[d.out_dtype == CTX_DTYPE_F32 ? 1 : 0][wgw];
+    if (per_cu == 0) {
       int64_t r[2];
-      rc = balanced_ranges(d, sd->cus, wgw, r);
+      rc = resident_waves(d.out_dtype, wgw, r);
       if (rc != CTX_OK) return rc;
-      ranges = (int32_t)r[0];
+      per_cu = r[0];
     }
+    // the same split as a handle made from this descriptor on this device
+    const int64_t ranges = ranges_for(sd->cus, per_cu, d.num_kv_heads);
     h.desc = d;
     h.device = dev;
     h.num_cus = sd->cus;
-    h.ranges_auto[0] = ranges;
+    h.ranges_auto[0] = (int32_t)ranges;
     h.ranges_auto[1] = 0;  // paged layout: not served here
     h.max_ranges = ranges;
     h.split_wgw = wgw;

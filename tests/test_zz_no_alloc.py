@@ -1,9 +1,10 @@
 """ctx_decode_attn_run_static (no handle, no allocation: the split workspace is
 the library's static device array) against ctx_decode_attn_run, through the C ABI.
 
-Two calls in a row, the second with a smaller batch, each bit for bit equal to
-the handle's run on the same inputs and within the parity gate of the oracle;
-then a call whose workspace would exceed the static array is refused."""
+Two calls in a row, the second with a smaller batch, then one with twice the
+KV heads, each bit for bit equal to the handle's run on the same inputs and
+within the parity gate of the oracle; then a call whose workspace would exceed
+the static array is refused."""
 import ctypes
 
 import numpy as np
@@ -40,26 +41,30 @@ def static_run(desc, q, k, v, offs, lens, scale, out):
 @pytest.mark.parametrize("out_dtype", [torch.float32, torch.bfloat16], ids=["f32", "bf16"])
 def test_static_entry_matches_the_handle_run(out_dtype):
     code = bd.CTX_DTYPE_F32 if out_dtype == torch.float32 else bd.CTX_DTYPE_BF16
-    # the first call is the larger one, so the second reuses a workspace holding stale partials
-    for seed, batch, lo, hi in [(1, 256, 16, 1200), (2, 37, 1, 900)]:
-        w, lay, q, k, v = case(seed, batch, 32, 8, lo, hi)
+    # The first call is the larger one, so the second reuses a workspace holding
+    # stale partials.  The third has twice the KV heads with the same workgroup
+    # shape: its split (ranges per KV head) must follow its own head count, as a
+    # handle's does, for the two results to agree bit for bit.
+    for seed, batch, lo, hi, hq, hkv in [(1, 256, 16, 1200, 32, 8), (2, 37, 1, 900, 32, 8),
+                                         (4, 40, 1, 900, 32, 16)]:
+        w, lay, q, k, v = case(seed, batch, hq, hkv, lo, hi)
         qd, kd, vd = up_bf16(q), up_bf16(k), up_bf16(v)
         offs, lens = up_i32(lay.offsets), up_i32(lay.lens)
-        desc = bd.CtxDesc(32, 8, 128, 256, int(lay.lens.max()), code, 0, 0)
-        buf = torch.full((batch + 1, 32, 128), -3.0, dtype=out_dtype, device=dev())
+        desc = bd.CtxDesc(hq, hkv, 128, 256, int(lay.lens.max()), code, 0, 0)
+        buf = torch.full((batch + 1, hq, 128), -3.0, dtype=out_dtype, device=dev())
         got = buf[:batch]
         assert static_run(desc, qd, kd, vd, offs, lens, w.scale, got) == bd.CTX_OK
         torch.cuda.synchronize()
         assert (buf[batch] == -3.0).all(), "write past the end of out"
-        with DecodeAttention(32, 8, 256, int(lay.lens.max()), out_dtype=out_dtype) as attn:
+        with DecodeAttention(hq, hkv, 256, int(lay.lens.max()), out_dtype=out_dtype) as attn:
             want = torch.empty_like(got)
             attn.run(qd, kd, vd, offs, lens, w.scale, want)
             torch.cuda.synchronize()
         assert torch.equal(got.view(torch.int16) if out_dtype == torch.bfloat16 else got.view(torch.int32),
                            want.view(torch.int16) if out_dtype == torch.bfloat16 else want.view(torch.int32)), \
-            f"static entry differs from the handle run (batch {batch})"
+            f"static entry differs from the handle run (batch {batch}, {hq}/{hkv} heads)"
         ref = oracle.decode_attn(q, k, v, lay.offsets, lay.lens, w.scale)
-        assert_parity(got.float().cpu().numpy(), ref, f"static entry, batch {batch}, {out_dtype}",
+        assert_parity(got.float().cpu().numpy(), ref, f"static entry, batch {batch}, {hq}/{hkv} heads, {out_dtype}",
                       tight=out_dtype == torch.float32)
 
 
