@@ -45,9 +45,10 @@ def test_measured_costs_are_physical(calibration):
     assert 50.0 < pf["tflops"] <= 2500.0, pf             # below the 2.5 PFLOP/s bf16 MFMA peak
     assert att["per_kv_token_s"] > 0.0 and att["achieved_gbs"] <= 8000.0, att
     # the line fits every measured point: the cost is linear in the KV tokens
+    # (within 15%, or 3 us, about one launch's jitter, at the smallest point)
     for p in att["points"]:
         fit = att["per_call_s"] + att["per_kv_token_s"] * p["kv_tokens"]
-        assert abs(fit - p["seconds"]) <= 0.15 * p["seconds"], (p, fit)
+        assert abs(fit - p["seconds"]) <= max(0.15 * p["seconds"], 3e-6), (p, fit)
     eng = calibration["engine"]
     assert all(np.isfinite(v) and v > 0 for v in eng.values()), eng
 
