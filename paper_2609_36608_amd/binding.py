@@ -323,7 +323,7 @@ def ctx_decode_attn_run_static(q, k_cache, v_cache, seq_offsets, seq_lens, scale
     """ctx_decode_attn_run_static: the decode step with no handle and no
     allocation (the split workspace is the library's static device array).
     q / out [B, Hq, 128] (out float32 or bfloat16), caches [rows, Hkv, 128] bf16,
-    seq_offsets / seq_lens [B] int32; max_batch defaults to B."""
+    seq_offsets / seq_lens [B] int32; max_batch defaults to B (1 for an empty batch)."""
     import torch
 
     lib = load_library()
@@ -338,7 +338,8 @@ def ctx_decode_attn_run_static(q, k_cache, v_cache, seq_offsets, seq_lens, scale
         raise ValueError(f"k_cache/v_cache must be [rows, {num_kv_heads}, 128]")
     if seq_offsets.shape != (b,) or seq_lens.shape != (b,):
         raise ValueError(f"seq_offsets/seq_lens must be [{b}]")
-    desc = CtxDesc(hq, num_kv_heads, q.shape[2], b if max_batch is None else max_batch, 1, _dtype_code(out.dtype), 0, 0)
+    desc = CtxDesc(hq, num_kv_heads, q.shape[2], max(b, 1) if max_batch is None else max_batch, 1,
+                   _dtype_code(out.dtype), 0, 0)
     rc = lib.ctx_decode_attn_run_static(ctypes.byref(desc), q.data_ptr(), k_cache.data_ptr(), v_cache.data_ptr(),
                                         seq_offsets.data_ptr(), seq_lens.data_ptr(), b, float(scale), out.data_ptr(),
                                         _stream_ptr(stream, q.device))

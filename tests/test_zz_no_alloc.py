@@ -77,6 +77,10 @@ def test_static_entry_python_binding_and_capacity():
     torch.cuda.synchronize()
     ref = oracle.decode_attn(q, k, v, lay.offsets, lay.lens, w.scale)
     assert_parity(out.cpu().numpy(), ref, "static entry through the binding")
+    # an empty batch is a no-op through the binding as through the C ABI
+    assert bd.ctx_decode_attn_run_static(qd[:0], kd, vd, offs[:0], lens[:0], w.scale, out[:0],
+                                         num_kv_heads=8).shape[0] == 0
+    torch.cuda.synchronize()
     # 128 query heads: even one sequence needs more than the static workspace holds
     big = torch.zeros((1, 128, 128), dtype=torch.bfloat16, device=dev())
     kv = torch.zeros((4, 8, 128), dtype=torch.bfloat16, device=dev())
