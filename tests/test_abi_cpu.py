@@ -118,3 +118,33 @@ def test_static_run_null_and_empty(lib):
                                           None) == bd.CTX_ERR_INVALID_ARG
     assert lib.ctx_decode_attn_run_static(ctypes.byref(good_desc()), 18, 16, 16, 16, 16, 1, 0.1, 16,
                                           None) == bd.CTX_ERR_ALIGNMENT
+
+
+@pytest.mark.parametrize("args,status", [
+    ((None, 16, 16, 1, 0), bd.CTX_ERR_INVALID_ARG),        # NULL source
+    ((16, 16, None, 1, 0), bd.CTX_ERR_INVALID_ARG),        # NULL sink / destination
+    ((16, 0, 16, 1, 0), bd.CTX_ERR_INVALID_ARG),           # no bytes
+    ((16, 24, 16, 1, 0), bd.CTX_ERR_INVALID_ARG),          # not whole 16-byte chunks
+    ((16, 16, 16, 0, 0), bd.CTX_ERR_INVALID_ARG),          # empty grid
+    ((16, 16, 16, 1, 2), bd.CTX_ERR_INVALID_ARG),          # unknown flag bit
+    ((24, 16, 16, 1, 0), bd.CTX_ERR_ALIGNMENT),            # misaligned source
+    ((16, 16, 8, 1, 0), bd.CTX_ERR_ALIGNMENT),             # misaligned sink / destination
+])
+def test_streaming_probes_reject_bad_arguments_before_the_device(lib, args, status):
+    src, nbytes, other, wg, flags = args
+    assert lib.ctx_hbm_read(src, nbytes, other, wg, flags, None) == status
+    assert lib.ctx_hbm_copy(src, other, nbytes, wg, flags, None) == status
+    assert lib.ctx_decode_attn_last_error().decode()
+
+
+@pytest.mark.parametrize("args,status", [
+    ((2, 1, 1, 16), bd.CTX_ERR_INVALID_ARG),               # unknown MFMA shape
+    ((bd.CTX_MFMA_16X16X32, 0, 1, 16), bd.CTX_ERR_INVALID_ARG),    # empty grid
+    ((bd.CTX_MFMA_32X32X16, 1, 0, 16), bd.CTX_ERR_INVALID_ARG),    # no iterations
+    ((bd.CTX_MFMA_16X16X32, 1, 1, None), bd.CTX_ERR_INVALID_ARG),  # NULL sink
+    ((bd.CTX_MFMA_16X16X32, 1, 1, 8), bd.CTX_ERR_ALIGNMENT),       # misaligned sink
+])
+def test_mfma_probe_rejects_bad_arguments_before_the_device(lib, args, status):
+    shape, wg, iters, sink = args
+    assert lib.ctx_mfma_bf16(shape, wg, iters, sink, None) == status
+    assert lib.ctx_decode_attn_last_error().decode()
