@@ -73,8 +73,9 @@ typedef struct {
  *                 seq_starts[num_seqs] = num_tokens
  *   params        HOST pointer, read during the call
  *   token_logp    float [num_tokens] out, lp_j (0 on masked rows), or NULL
- *   token_weight  float [num_tokens] out, w_j (required)
- *   token_loss    float [num_tokens] out, l_j (0 on masked rows; required)
+ *   token_weight  float [num_tokens] out, w_j (required when num_tokens > 0)
+ *   token_loss    float [num_tokens] out, l_j (0 on masked rows; required when
+ *                 num_tokens > 0)
  *   loss          float [1] out, the batch loss (0 for an empty batch)
  *   grad_logits   bf16 [num_tokens, grad_row_stride] out, or NULL for the
  *                 loss alone; columns >= vocab are not written

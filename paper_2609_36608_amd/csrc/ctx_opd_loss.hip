@@ -391,8 +391,10 @@ extern "C" int ctx_opd_loss_run(const void* logits, int64_t row_stride, int32_t 
   if (vocab > kMaxVocab) return fail(CTX_ERR_UNSUPPORTED, "vocab %d > %lld", vocab, (long long)kMaxVocab);
   if (row_stride < vocab || row_stride % kChunk != 0)
     return fail(CTX_ERR_INVALID_ARG, "row_stride %lld must be >= vocab and a multiple of 8", (long long)row_stride);
-  if (loss == nullptr || token_weight == nullptr || token_loss == nullptr || seq_starts == nullptr)
-    return fail(CTX_ERR_INVALID_ARG, "NULL loss, token_weight, token_loss or seq_starts");
+  if (loss == nullptr || seq_starts == nullptr) return fail(CTX_ERR_INVALID_ARG, "NULL loss or seq_starts");
+  // per-token arrays of an empty batch are never touched and may be NULL
+  if (num_tokens > 0 && (token_weight == nullptr || token_loss == nullptr))
+    return fail(CTX_ERR_INVALID_ARG, "NULL token_weight or token_loss");
   if (num_tokens > 0 && (logits == nullptr || tokens == nullptr || old_logp == nullptr ||
                          teacher_logp == nullptr || mask == nullptr))
     return fail(CTX_ERR_INVALID_ARG, "NULL per-token input");

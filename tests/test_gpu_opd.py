@@ -197,5 +197,10 @@ def test_opd_abi_errors():
     assert call(weight=None) == bd.CTX_ERR_INVALID_ARG
     assert call(nseq=0) == bd.CTX_ERR_INVALID_ARG            # tokens without responses
     assert call(grad=None) == bd.CTX_OK
+    # an empty batch: the per-token arrays may be NULL; only loss and seq_starts are needed
+    st0 = torch.zeros(2, dtype=torch.int32, device=dev())  # one empty response
+    assert lib.ctx_opd_loss_run(None, vocab, vocab, None, None, None, None, P(st0), 1, 0, ctypes.byref(good),
+                                None, None, None, P(loss), None, 0, None) == bd.CTX_OK
     torch.cuda.synchronize()
+    assert float(loss.cpu()[0]) == 0.0
     assert bd.load_library().ctx_decode_attn_last_error() is not None
